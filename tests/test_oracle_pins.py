@@ -1,0 +1,501 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+None of these tests retypes the oracle's own formulas: each checks the oracle
+against an independent statement -- a closed form, a geometric construction
+done here from scratch (separating axes, polygon containment), exact rational
+arithmetic, a library routine (scipy's nearest-codeword search), brute force
+over tiny inputs, or a value the paper prints (tests/golden/paper_facts.json).
+"""
+import itertools
+import json
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.filterwarnings("ignore")
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "paper_facts.json")
+
+
+@pytest.fixture(scope="module")
+def facts():
+    with open(GOLDEN) as f:
+        return json.load(f)
+
+
+# ------------------------------------------------------------------ geometry helpers (test-only)
+
+def ngon(N):
+    """Regular N-gon, unit circumradius, vertex c at angle 2*pi*c/N (counter-clockwise)."""
+    t = 2.0 * np.pi * np.arange(N) / N
+    return np.stack([np.cos(t), np.sin(t)], axis=1)
+
+
+def cells_disjoint_sat(N, r):
+    """True when every pair of cells (1-r)V(a) + r*hull is separated, by the separating-axis
+    theorem on the hull's edge normals (both cells are translates of the same convex polygon)."""
+    V = ngon(N)
+    E = np.roll(V, -1, axis=0) - V
+    n = np.stack([-E[:, 1], E[:, 0]], axis=1)
+    n /= np.linalg.norm(n, axis=1, keepdims=True)
+    proj = V @ n.T                          # [vertex][axis]
+    width = proj.max(0) - proj.min(0)       # extent of the hull along each axis
+    C = (1.0 - r) * V
+    for a in range(N):
+        for b in range(a + 1, N):
+            sep = np.abs((C[a] - C[b]) @ n.T) - r * width
+            if not (sep.max() > 0.0):
+                return False
+    return True
+
+
+def inside_convex(poly, q, eps=1e-12):
+    """Point in a counter-clockwise convex polygon (boundary counts as inside)."""
+    a = poly
+    b = np.roll(poly, -1, axis=0)
+    cr = (b[:, 0] - a[:, 0]) * (q[1] - a[:, 1]) - (b[:, 1] - a[:, 1]) * (q[0] - a[:, 0])
+    return bool(np.all(cr >= -eps))
+
+
+def cell_polygon(N, r, c):
+    V = ngon(N)
+    return (1.0 - r) * V[c] + r * V
+
+
+# ------------------------------------------------------------------ a1: codec parameters
+
+def test_midpoint_is_boundary_for_small_alphabets(orc, facts):
+    f = facts["midpoint_boundary"]
+    for N in f["N"]:
+        assert orc.r_max(N) == pytest.approx(f["r_N"], abs=1e-15)
+    for N in range(5, 40):
+        assert orc.r_max(N) < 0.5, "larger alphabets must be tightened below the midpoint ratio"
+
+
+def test_r_max_equals_nflake_closed_form(orc):
+    # Independent closed form for the n-flake ratio: 1 / (2 (1 + sum_{k=1}^{floor(N/4)} cos(2 pi k / N))).
+    for N in range(3, 1025):
+        nf = 1.0 / (2.0 * (1.0 + sum(math.cos(2.0 * math.pi * k / N) for k in range(1, N // 4 + 1))))
+        assert abs(orc.r_max(N) - nf) < 1e-15, N
+
+
+def test_r_max_equals_sat_bisection(orc):
+    for N in list(range(3, 17)) + [24, 32, 64]:
+        lo, hi = 0.0, 0.6
+        for _ in range(60):
+            mid = 0.5 * (lo + hi)
+            if cells_disjoint_sat(N, mid):
+                lo = mid
+            else:
+                hi = mid
+        assert abs(orc.r_max(N) - lo) < 1e-9, (N, orc.r_max(N), lo)
+
+
+def test_working_ratio_disjoint_and_limit_is_tight(orc):
+    for N in (3, 4, 5, 6, 7, 8, 16, 64):
+        c = orc.Codec(N, 0.98)
+        assert cells_disjoint_sat(N, c.r)
+        assert not cells_disjoint_sat(N, 1.001 * c.r_max), "cells must meet just above r_N"
+
+
+def test_vertex_table_orientation(orc):
+    c = orc.Codec(3, r_scale=1.0)
+    s3 = math.sqrt(3.0) / 2.0
+    want = np.array([[1.0, 0.0], [-0.5, s3], [-0.5, -s3]])
+    assert np.max(np.abs(c.V - want)) <= 2 * 2.0 ** -52
+    assert np.max(np.abs(c.W - 0.5 * c.V)) == 0.0
+    for N in (16, 64, 256):
+        c = orc.Codec(N)
+        assert np.max(np.abs(np.hypot(c.V[:, 0], c.V[:, 1]) - 1.0)) < 4e-16
+        ang = np.mod(np.arctan2(c.V[:, 1], c.V[:, 0]), 2 * np.pi)
+        assert np.max(np.abs(ang - 2 * np.pi * np.arange(N) / N)) < 1e-14 * N
+
+
+def test_span_length_from_capacity(orc, facts):
+    bits = facts["capacity_bits"]["value"]
+    expect = {16: 16, 64: 9, 256: 6}
+    for N, L in expect.items():
+        c = orc.Codec(N)
+        assert c.L == L
+        assert c.L == math.floor(bits / math.log2(1.0 / c.r))
+    assert orc.Codec(3, r_scale=1.0).L == 44 and orc.Codec(4, r_scale=1.0).L == 44
+    assert orc.Codec(16).r == pytest.approx(0.1625924674, abs=1e-10)
+    assert orc.Codec(64).r == pytest.approx(0.0458898872, abs=1e-10)
+    assert orc.Codec(256).r == pytest.approx(0.0118812015, abs=1e-10)
+
+
+def test_fig1_midpoint_cells(orc, facts):
+    """Fig. 1: at r = 1/2, N=3 leaves gaps, N=4 tiles, N>4 overlaps; the oracle's cell choice
+    is a cell that contains the point whenever one does."""
+    rng = np.random.default_rng(0)
+    assert facts["fig1_midpoint_cells"]["cell_area_fraction"] == 0.25
+    for N, expect in ((3, "gaps"), (4, "tiles"), (5, "overlaps"), (6, "overlaps")):
+        c = orc.Codec(N, r_scale=0.5 / orc.r_max(N))
+        assert c.r == 0.5
+        H = ngon(N)
+        polys = [cell_polygon(N, 0.5, k) for k in range(N)]
+        n_none = n_multi = 0
+        pts = rng.uniform(-1, 1, size=(4000, 2))
+        for q in pts:
+            if not inside_convex(H, q):
+                continue
+            hits = [k for k in range(N) if inside_convex(polys[k], q, eps=-1e-9)]
+            if not hits:
+                n_none += 1
+            elif len(hits) > 1:
+                n_multi += 1
+            if hits:
+                got = orc.cell(c, q[0], q[1])
+                assert inside_convex(polys[got], q, eps=1e-9)
+        if expect == "gaps":
+            assert n_none > 0 and n_multi == 0
+        elif expect == "tiles":
+            assert n_none == 0 and n_multi == 0
+        else:
+            assert n_multi > 0
+
+
+# ------------------------------------------------------------------ a3: encode
+
+def test_sierpinski_repeated_zero_exact(orc, facts):
+    f = facts["sierpinski_repeat_zero"]
+    c = orc.Codec(3, r_scale=1.0)
+    for k in range(1, 61):
+        p = orc.encode(c, np.zeros((1, k), np.uint8)) if k <= c.L else None
+        if p is None:
+            cc = orc.Codec(3, r_scale=1.0, L_override=k)
+            p = orc.encode(cc, np.zeros((1, k), np.uint8))
+        assert p[0, -1, 0] == 1.0 - 2.0 ** -k and p[0, -1, 1] == 0.0, k
+        if k <= len(f["points_x"]):
+            assert p[0, -1, 0] == f["points_x"][k - 1] and p[0, -1, 1] == f["points_y"][k - 1]
+
+
+def test_sierpinski_closed_forms(orc):
+    ulp = 2.0 ** -52
+    for m in range(1, 20):
+        c = orc.Codec(3, r_scale=1.0, L_override=2 * m)
+        seq = np.array([0, 1] * m, np.uint8)[None]
+        p = orc.encode(c, seq)[0, 0]
+        want = (1.0 - 4.0 ** -m) * (c.V[0] + 2.0 * c.V[1]) / 3.0
+        assert np.max(np.abs(p - want)) <= 4 * ulp
+    for k in range(1, 30):
+        c = orc.Codec(3, r_scale=1.0, L_override=k)
+        for sym in (1, 2):
+            p = orc.encode(c, np.full((1, k), sym, np.uint8))[0, 0]
+            assert np.max(np.abs(p - (1.0 - 2.0 ** -k) * c.V[sym])) <= 4 * ulp
+
+
+@pytest.mark.parametrize("N,scale", [(3, None), (3, 0.98), (16, 0.98), (64, 0.98), (256, 0.98)])
+def test_encode_equals_exact_rational_sum(orc, N, scale):
+    """p_L = sum_k (1-r) r^(L-k) V(c_k) from the anchor (0,0), evaluated exactly in rationals on
+    the fp64 table values; the fp64 recurrence must agree to a few ulp."""
+    rng = np.random.default_rng(N)
+    c = orc.Codec(N, r_scale=(1.0 / orc.r_max(N)) * 0.5 if scale is None else scale)
+    r = Fraction(c.r)
+    Vx = [Fraction(float(v)) for v in c.V[:, 0]]
+    Vy = [Fraction(float(v)) for v in c.V[:, 1]]
+    for L in (1, 2, 5, c.L):
+        cc = orc.Codec(N, r_scale=c.r / c.r_max, L_override=L, r=c.r)
+        seqs = rng.integers(0, N, size=(40, L), dtype=np.uint8)
+        pts = orc.encode(cc, seqs.reshape(1, -1))[0]
+        for i in range(40):
+            ex = Fraction(0)
+            ey = Fraction(0)
+            for k in range(L):
+                w = (1 - r) * r ** (L - 1 - k)
+                ex += w * Vx[seqs[i, k]]
+                ey += w * Vy[seqs[i, k]]
+            assert abs(pts[i, 0] - float(ex)) <= 4 * 2.0 ** -52
+            assert abs(pts[i, 1] - float(ey)) <= 4 * 2.0 ** -52
+
+
+def test_partial_last_span_and_anchor(orc):
+    c = orc.Codec(16)
+    rng = np.random.default_rng(3)
+    n = 3 * c.L + 5
+    sym = rng.integers(0, 16, size=(2, n), dtype=np.uint8)
+    pts = orc.encode(c, sym)
+    assert pts.shape == (2, 4, 2)
+    # each span is encoded from the anchor (0,0): encoding a span alone gives the same point
+    for j in range(4):
+        seg = sym[:, j * c.L:(j + 1) * c.L]
+        cc = orc.Codec(16, L_override=seg.shape[1])
+        assert np.array_equal(orc.encode(cc, seg)[:, 0], pts[:, j])
+
+
+@pytest.mark.parametrize("N", [3, 16, 64, 256])
+def test_decay_law(orc, facts, N):
+    """Sec. 5: positions sharing an s-symbol suffix are within 2 r^s."""
+    rng = np.random.default_rng(100 + N)
+    k = facts["decay_law"]["bound_factor"]
+    c = orc.Codec(N)
+    n = c.L
+    worst = 0.0
+    for s in range(0, n + 1):
+        A = rng.integers(0, N, size=(200, n), dtype=np.uint8)
+        B = rng.integers(0, N, size=(200, n), dtype=np.uint8)
+        if s:
+            B[:, n - s:] = A[:, n - s:]
+        cc = orc.Codec(N, L_override=n)
+        pa = orc.encode(cc, A.reshape(1, -1))[0]
+        pb = orc.encode(cc, B.reshape(1, -1))[0]
+        dist = np.hypot(pa[:, 0] - pb[:, 0], pa[:, 1] - pb[:, 1])
+        bound = k * c.r ** s
+        assert np.all(dist <= bound + 8 * 2.0 ** -52), (s, dist.max(), bound)
+        worst = max(worst, float(dist.max() / bound))
+    assert worst > 0.3  # the bound is not vacuous
+
+
+# ------------------------------------------------------------------ a4: decode
+
+@pytest.mark.parametrize("N", [3, 4, 5, 6])
+def test_roundtrip_bruteforce_small_alphabets(orc, N):
+    """Lossless round trip (Sec. 1, Sec. 2) over every sequence of length 1..8 (1..7 for N=6)."""
+    maxlen = 7 if N == 6 else 8
+    for scale in (0.98, 1.0):
+        for L in range(1, maxlen + 1):
+            c = orc.Codec(N, r_scale=scale, L_override=L)
+            allseq = np.array(list(itertools.product(range(N), repeat=L)), np.uint8).reshape(1, -1)
+            pts = orc.encode(c, allseq)
+            dec, ok, nf, _ = orc.decode(c, pts, allseq.shape[1], verify=True)
+            assert nf == 0 and ok.all()
+            assert np.array_equal(dec, allseq), (N, scale, L)
+
+
+@pytest.mark.parametrize("N", [16, 64, 256])
+def test_roundtrip_random_spans(orc, N):
+    rng = np.random.default_rng(N)
+    c = orc.Codec(N)
+    n = 5000 * c.L + 3
+    sym = rng.integers(0, N, size=(3, n), dtype=np.uint8)
+    pts = orc.encode(c, sym)
+    dec, ok, nf, res = orc.decode(c, pts, n, verify=True)
+    assert nf == 0 and np.array_equal(dec, sym)
+    assert res.max() < 2.0 ** -6
+
+
+@pytest.mark.parametrize("N,r_scale", [(3, None), (16, 0.98), (64, 0.98), (256, 0.98)])
+def test_capacity_sweep(orc, N, r_scale):
+    """Sec. 1: about 44/log2(1/r) symbols per double.  Zero round-trip failures at
+    L = floor(44/log2(1/r)) over many random spans; the first failing L lies in
+    [floor(50/log2(1/r)), ceil(54/log2(1/r)) + 1] (the floor leaves some bits of headroom)."""
+    rs = (0.5 / orc.r_max(N)) if r_scale is None else r_scale
+    base = orc.Codec(N, r_scale=rs)
+    lg = math.log2(1.0 / base.r)
+    rng = np.random.default_rng(7 * N)
+    n_spans = 200000 if N <= 16 else 100000
+
+    def failures(L):
+        c = orc.Codec(N, r_scale=rs, L_override=L)
+        sym = rng.integers(0, N, size=(1, n_spans * L), dtype=np.uint8)
+        dec, _, _, _ = orc.decode(c, orc.encode(c, sym), sym.shape[1])
+        return int(np.any((dec != sym).reshape(n_spans, L), axis=1).sum())
+
+    assert failures(base.L) == 0
+    first = None
+    for L in range(base.L + 1, base.L + 40):
+        if failures(L) > 0:
+            first = L
+            break
+    assert first is not None
+    assert math.floor(50 / lg) <= first <= math.ceil(54 / lg) + 1, (first, 50 / lg, 54 / lg)
+
+
+@pytest.mark.parametrize("N", [3, 4, 5, 6, 7, 8])
+def test_nearest_centre_is_cell_membership(orc, N):
+    """Sec. 1: the decoded symbol is the vertex whose contracted image contains the point.
+    Walk random valid points backward and check every choice by polygon containment."""
+    rng = np.random.default_rng(N)
+    c = orc.Codec(N)
+    polys = [cell_polygon(N, c.r, k) for k in range(N)]
+    L = min(c.L, 12)
+    cc = orc.Codec(N, L_override=L)
+    seqs = rng.integers(0, N, size=(300, L), dtype=np.uint8)
+    pts = orc.encode(cc, seqs.reshape(1, -1))[0]
+    for i in range(300):
+        q = pts[i].copy()
+        for k in range(L - 1, -1, -1):
+            got = orc.cell(cc, q[0], q[1])
+            assert got == seqs[i, k]
+            assert inside_convex(polys[got], q, eps=1e-9)
+            q = (q - cc.W[got]) / cc.r
+
+
+def test_cell_exact_tie_takes_lowest_index(orc):
+    """Reading: an exact distance tie between cell centres goes to the lowest symbol.  For N=4 the
+    origin is at the same fp64 distance (1-r)^2 from all four centres."""
+    c = orc.Codec(4)
+    d = [(0.0 - c.W[k, 0]) ** 2 + (0.0 - c.W[k, 1]) ** 2 for k in range(4)]
+    assert len(set(d)) == 1
+    assert orc.cell(c, 0.0, 0.0) == 0
+
+
+def test_failure_detection(orc):
+    c = orc.Codec(64)
+    rng = np.random.default_rng(5)
+    n = 40 * c.L
+    sym = rng.integers(0, 64, size=(1, n), dtype=np.uint8)
+    pts = orc.encode(c, sym)
+    bad = pts.copy()
+    bad[0, 0, 0] = np.nextafter(bad[0, 0, 0], 2.0)   # 1 ulp: anchor passes, re-encode does not
+    bad[0, 1, 0] += 1e-3                              # far off: anchor fails
+    bad[0, 2] = (3.0, 0.0)                            # outside the hull
+    bad[0, 3, 1] = np.nan
+    bad[0, 4, 0] = np.inf
+    dec, ok, nf, _ = orc.decode(c, bad, n, verify=False)
+    assert ok[0, 0] == 1 and np.array_equal(dec[0, :c.L], sym[0, :c.L])
+    assert list(ok[0, 1:5]) == [0, 0, 0, 0] and nf == 4
+    assert ok[0, 5:].all()
+    dec, ok, nf, _ = orc.decode(c, bad, n, verify=True)
+    assert ok[0, 0] == 0 and nf == 5
+
+
+# ------------------------------------------------------------------ a5: lookup
+
+def test_lookup_equals_bulk_slices(orc):
+    rng = np.random.default_rng(11)
+    for N, S in ((256, 2), (256, 4), (64, 2), (16, 2), (16, 3)):
+        c = orc.Codec(N)
+        Ta = 97
+        n = Ta * S
+        sym = rng.integers(0, N, size=(5, n), dtype=np.uint8)
+        pts = orc.encode(c, sym)
+        qs = rng.integers(0, 6, size=4000).astype(np.uint32)      # stream 5 is out of range
+        qt = rng.integers(0, Ta + 3, size=4000).astype(np.uint32)  # tokens >= Ta are out of range
+        out, st, nf = orc.lookup(c, pts, n, S, qs, qt)
+        for i in range(4000):
+            if qs[i] >= 5 or qt[i] >= Ta:
+                assert st[i] == 2 and not out[i].any()
+            else:
+                assert st[i] == 0
+                assert np.array_equal(out[i], sym[qs[i], qt[i] * S:(qt[i] + 1) * S])
+        assert nf == int((st != 0).sum())
+
+
+# ------------------------------------------------------------------ a2: residual VQ
+
+def test_half_to_double_every_pattern(orc):
+    for h in range(0, 65536, 1):
+        want = np.array([h], np.uint16).view(np.float16).astype(np.float64)[0]
+        got = orc.half_to_double(h)
+        if np.isnan(want):
+            assert math.isnan(got)
+        else:
+            assert got == want, hex(h)
+
+
+def _rand_books(rng, nb, S, K, d):
+    b = rng.standard_normal((nb, S, K, d)).astype(np.float32)
+    b *= (0.5 ** np.arange(S))[None, :, None, None]
+    return b.astype(np.float16)
+
+
+def test_rvq_single_stage_is_nearest_codeword(orc):
+    from scipy.cluster.vq import vq
+    rng = np.random.default_rng(21)
+    ns, T, d, K = 3, 300, 64, 256
+    x = rng.standard_normal((ns, T, d)).astype(np.float16)
+    books = _rand_books(rng, 2, 1, K, d)
+    sb = np.array([0, 1, 1], np.int32)
+    out = orc.rvq_assign(x, books, sb, 10, 290)
+    for s in range(ns):
+        obs = x[s, 10:290].astype(np.float64)
+        cb = books[sb[s], 0].astype(np.float64)
+        code, dist = vq(obs, cb, check_finite=False)
+        assert np.array_equal(out["symbols"][s], code.astype(np.uint8))
+        assert np.allclose(out["residual"][s], obs - cb[code], atol=0, rtol=0)
+
+
+def test_rvq_each_stage_is_nearest_codeword_of_its_residual(orc):
+    from scipy.cluster.vq import vq
+    rng = np.random.default_rng(22)
+    ns, T, d, S, K = 2, 200, 64, 3, 64
+    x = (rng.standard_normal((ns, T, d)) * 2).astype(np.float16)
+    books = _rand_books(rng, ns, S, K, d)
+    sb = np.arange(ns, dtype=np.int32)
+    out = orc.rvq_assign(x, books, sb, 0, T)
+    sym = out["symbols"].reshape(ns, T, S)
+    for s in range(ns):
+        r = x[s].astype(np.float64)
+        for st in range(S):
+            cb = books[s, st].astype(np.float64)
+            code, _ = vq(r, cb, check_finite=False)
+            assert np.array_equal(sym[s, :, st], code)
+            r = r - cb[code]
+        assert np.array_equal(out["residual"][s], r)  # exact: sums of a few fp16 values
+
+
+def test_rvq_special_cases(orc):
+    rng = np.random.default_rng(23)
+    d, K = 32, 16
+    books = _rand_books(rng, 1, 2, K, d)
+    # x equal to a codeword: that codeword, distance 0, zero residual after stage 0 then stage 1
+    x = books[0, 0][[5, 9, 0]][None].copy()
+    out = orc.rvq_assign(x, books[:, :1], np.zeros(1, np.int32), 0, 3)
+    assert list(out["symbols"][0]) == [5, 9, 0]
+    assert not out["residual"].any()
+    # K = 1: all indices zero, residual x - sum of the single codewords
+    b1 = books[:, :, :1]
+    x = rng.standard_normal((1, 7, d)).astype(np.float16)
+    out = orc.rvq_assign(x, b1, np.zeros(1, np.int32), 0, 7)
+    assert not out["symbols"].any()
+    want = x[0].astype(np.float64) - b1[0, 0, 0].astype(np.float64) - b1[0, 1, 0].astype(np.float64)
+    assert np.array_equal(out["residual"][0], want)
+    # duplicate codewords: lowest index wins, and the reported gap is 0
+    bd = books.copy()
+    bd[0, 0, 11] = bd[0, 0, 3]
+    x = bd[0, 0, [3]][None].copy()
+    out = orc.rvq_assign(x, bd[:, :1], np.zeros(1, np.int32), 0, 1)
+    assert out["symbols"][0, 0] == 3 and out["gaps"][0, 0, 0] == 0.0
+
+
+def test_rvq_permutation_equivariance(orc):
+    rng = np.random.default_rng(24)
+    d, K, T = 64, 128, 400
+    books = _rand_books(rng, 1, 1, K, d)
+    x = rng.standard_normal((1, T, d)).astype(np.float16)
+    perm = rng.permutation(K)
+    a = orc.rvq_assign(x, books, np.zeros(1, np.int32), 0, T)["symbols"][0]
+    b = orc.rvq_assign(x, books[:, :, perm], np.zeros(1, np.int32), 0, T)["symbols"][0]
+    assert np.array_equal(perm[b], a)
+
+
+def test_rvq_gap_and_teacher_forcing(orc):
+    d = 16
+    books = np.zeros((1, 2, 3, d), np.float16)
+    books[0, 0, 0, 0] = 1.0        # D = 1
+    books[0, 0, 1, 1] = -1.0       # D = 1 (exact tie with 0)
+    books[0, 0, 2, 2] = 1.25       # D = 1.5625
+    books[0, 1, :, 3] = [0.5, 0.25, 2.0]
+    x = np.zeros((1, 1, d), np.float16)
+    out = orc.rvq_assign(x, books, np.zeros(1, np.int32), 0, 1)
+    assert list(out["symbols"][0]) == [0, 1]
+    assert out["gaps"][0, 0, 0] == 0.0
+    r1 = np.zeros(d); r1[0] = -1.0
+    D = [np.sum((r1 - books[0, 1, j].astype(np.float64)) ** 2) for j in range(3)]
+    assert out["gaps"][0, 0, 1] == pytest.approx((sorted(D)[1] - sorted(D)[0]) / sorted(D)[1])
+    # forcing the tied alternative is accepted and changes the next stage's residual
+    f = np.array([[1, 1]], np.uint8)
+    o2 = orc.rvq_assign(x, books, np.zeros(1, np.int32), 0, 1, force=f)
+    assert o2["n_forced"] == 1 and o2["n_hard"] == 0 and list(o2["symbols"][0]) == [1, 1]
+    # forcing a clearly worse codeword is refused and counted as a hard disagreement
+    f = np.array([[2, 1]], np.uint8)
+    o3 = orc.rvq_assign(x, books, np.zeros(1, np.int32), 0, 1, force=f)
+    assert o3["n_hard"] == 1 and o3["symbols"][0, 0] == 0
+
+
+# ------------------------------------------------------------------ window and sizes
+
+def test_window_and_sizes(facts):
+    from paper_2607_07144_amd import workloads as w
+    win = facts["exact_window"]
+    assert (w.SINKS, w.RECENT) == (win["sinks"], win["recent"])
+    assert w.CONFIGS["tiny"].T_arch == 220
+    g = w.CONFIGS["gpt2"]
+    assert g.T == win["context"] and g.T_arch == 988
+    assert round(100 * (w.SINKS + w.RECENT) / g.T, 1) == win["exact_percent"]
+    assert g.scalars_per_token() == facts["gpt2_kv_scalars_per_token"]["value"]
+    assert 2 * g.scalars_per_token() == facts["fp16_bytes_per_token"]["value"]
