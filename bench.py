@@ -1,0 +1,263 @@
+#!/usr/bin/env python3
+"""Throughput of the fractal KV-archive hot path on one MI355X.
+
+One step is one pass of the whole path over one batch of synthetic K/V:
+residual-VQ assignment of every archived head vector, fixed-span encode of the
+resulting symbol streams, bulk decode of every span, and a batch of random
+O(1) lookups.  Inputs are resident in device memory before the timed region.
+
+Prints one JSON line.  `value` is archived tokens per second over the whole
+step (a token is one position across all layers, heads and K/V); per-phase
+rates, the dominant kernel's roofline fraction and the CPU oracle's rate on the
+same workload are reported beside it.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_FP16_MFMA_TFLOPS = 2500.0   # MI355X dense fp16 matrix peak
+PEAK_HBM_GBS = 8000.0            # MI355X HBM3E bandwidth
+METRIC = "archived tokens/s (RVQ assign + CGR encode) and decoded symbols/s, 1 MI355X"
+
+
+def source_hash(*names):
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(ROOT, "paper_2607_07144_amd", "csrc", n), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+KERNEL_SOURCES = {
+    "rvq_assign": ("rvq_kernels.hip", "fkv_hip_common.h"),
+    "cgr_encode": ("cgr_kernels.hip", "fkv_hip_common.h", "fkv_internal.h"),
+    "cgr_decode": ("cgr_kernels.hip", "fkv_hip_common.h", "fkv_internal.h"),
+    "span_lookup": ("cgr_kernels.hip", "fkv_hip_common.h", "fkv_internal.h"),
+}
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or None when absent or
+    taken on a different version of the kernel's source."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path)).get(workload, {}).get(kernel)
+    except (OSError, ValueError):
+        return None
+    if not rec or rec.get("source_hash") != source_hash(*KERNEL_SOURCES[kernel]):
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def build_workload(name: str, n_lookups: int):
+    import torch
+    from paper_2607_07144_amd import fkv, workloads
+
+    cfg = workloads.CONFIGS[name]
+    groups = []
+    for gi, g in enumerate(cfg.groups):
+        if name == "long_gqa":
+            x, books, sb = workloads.make_group_torch(cfg, gi)
+            host = None
+        else:
+            xh, bh, sbh = workloads.make_group_numpy(cfg, gi)
+            x, books, sb = (torch.from_numpy(a).cuda() for a in (xh, bh, sbh))
+            host = (xh, bh, sbh)
+        ns = x.shape[0]
+        codec = fkv.Codec(g.N, g.r_scale)
+        n_sym = cfg.T_arch * g.S
+        n_spans = codec.n_spans(n_sym)
+        rng = np.random.default_rng(cfg.seed + 17 * gi)
+        qs = rng.integers(0, ns, size=n_lookups).astype(np.int32)
+        qt = rng.integers(0, cfg.T_arch, size=n_lookups).astype(np.int32)
+        groups.append(dict(
+            g=g, codec=codec, x=x, books=books, sb=sb, host=host, ns=ns, n_sym=n_sym, n_spans=n_spans,
+            sym=torch.empty((ns, n_sym), dtype=torch.uint8, device="cuda"),
+            pts=torch.empty((ns, n_spans, 2), dtype=torch.float64, device="cuda"),
+            dec=torch.empty((ns, n_sym), dtype=torch.uint8, device="cuda"),
+            qs=torch.from_numpy(qs).cuda(), qt=torch.from_numpy(qt).cuda(), qs_h=qs, qt_h=qt,
+            out=torch.empty((n_lookups, g.S), dtype=torch.uint8, device="cuda"),
+        ))
+    return cfg, groups
+
+
+def run_step(fkv, cfg, groups, ev=None):
+    for gr in groups:
+        if ev is not None:
+            ev["rvq_assign"][0].record()
+        fkv.fkv_rvq_assign(gr["x"], gr["books"], gr["sb"], cfg.t_begin, cfg.t_end, symbols=gr["sym"])
+        if ev is not None:
+            ev["rvq_assign"][1].record()
+            ev["cgr_encode"][0].record()
+        fkv.fkv_cgr_encode_spans(gr["codec"], gr["sym"], points=gr["pts"])
+        if ev is not None:
+            ev["cgr_encode"][1].record()
+            ev["cgr_decode"][0].record()
+        fkv.fkv_cgr_decode_spans(gr["codec"], gr["pts"], gr["n_sym"], symbols=gr["dec"])
+        if ev is not None:
+            ev["cgr_decode"][1].record()
+            ev["span_lookup"][0].record()
+        fkv.fkv_span_lookup(gr["codec"], gr["pts"], gr["n_sym"], gr["g"].S, gr["qs"], gr["qt"], out=gr["out"])
+        if ev is not None:
+            ev["span_lookup"][1].record()
+
+
+def algorithmic(cfg, groups):
+    """Algorithmic FLOPs / bytes per launch of each kernel, summed over groups."""
+    a = {"rvq_assign": {"flops": 0, "bytes": 0}, "cgr_encode": {"bytes": 0}, "cgr_decode": {"bytes": 0},
+         "span_lookup": {"bytes": 0}, "symbols": 0, "lookups": 0, "head_vectors": 0}
+    for gr in groups:
+        g, ns, d = gr["g"], gr["ns"], cfg.d
+        nb = gr["books"].shape[0]
+        a["rvq_assign"]["flops"] += ns * cfg.T_arch * g.S * 2 * g.K * d
+        a["rvq_assign"]["bytes"] += ns * cfg.T_arch * d * 2 + nb * g.S * g.K * d * 2 + ns * cfg.T_arch * g.S
+        codec_bytes = ns * gr["n_sym"] + ns * gr["n_spans"] * 16
+        a["cgr_encode"]["bytes"] += codec_bytes
+        a["cgr_decode"]["bytes"] += codec_bytes
+        L = gr["codec"].L
+        qt = gr["qt_h"].astype(np.int64) * g.S
+        spans_touched = (qt + g.S - 1) // L - qt // L + 1
+        a["span_lookup"]["bytes"] += int(gr["qs_h"].size * (8 + g.S) + 16 * spans_touched.sum())
+        a["symbols"] += ns * gr["n_sym"]
+        a["lookups"] += gr["qs_h"].size
+        a["head_vectors"] += ns * cfg.T_arch
+    return a
+
+
+def cpu_baseline(cfg, groups, max_streams: int):
+    """The CPU oracle on (a sample of) the same step, all host cores, extrapolated per token."""
+    import oracle
+
+    threads = oracle.default_threads()
+    t_total = 0.0
+    frac = []
+    for gr in groups:
+        if gr["host"] is None:
+            return None
+        xh, bh, sbh = gr["host"]
+        ns = min(gr["ns"], max_streams)
+        t0 = time.perf_counter()
+        o = oracle.rvq_assign(xh[:ns], bh, sbh[:ns], cfg.t_begin, cfg.t_end, want_residual=False,
+                              want_gaps=False, threads=threads)
+        oc = oracle.Codec(gr["g"].N, gr["g"].r_scale)
+        pts = oracle.encode(oc, o["symbols"], threads=threads)
+        oracle.decode(oc, pts, gr["n_sym"], threads=threads)
+        keep = gr["qs_h"] < ns
+        oracle.lookup(oc, pts, gr["n_sym"], gr["g"].S, gr["qs_h"][keep].astype(np.uint32),
+                      gr["qt_h"][keep].astype(np.uint32), threads=threads)
+        t_total += (time.perf_counter() - t0) * gr["ns"] / ns
+        frac.append("%d/%d streams" % (ns, gr["ns"]))
+    return {"value": cfg.batch * cfg.T_arch / t_total, "unit": "archived tokens/s", "cores": threads,
+            "kind": "oracle",
+            "sample": "%s of %s (full step: RVQ, encode, decode, lookups on the sampled streams), "
+                      "time scaled to all streams" % (", ".join(frac), cfg.name)}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="gpt2",
+                    choices=["gpt2", "tiny", "gpt2_hybrid_b16", "long_gqa"])
+    ap.add_argument("--lookups", type=int, default=1 << 16)
+    ap.add_argument("--cpu-streams", type=int, default=288,
+                    help="streams per group the CPU oracle baseline runs on")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures the path on one GPU; multi-GPU runs are not part of this build "
+              "(streams shard with no exchange, see DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2607_07144_amd import fkv
+
+    torch.cuda.set_device(0)
+    cfg, groups = build_workload(args.workload, args.lookups)
+    torch.cuda.synchronize()
+    for _ in range(args.warmup):
+        run_step(fkv, cfg, groups)
+    torch.cuda.synchronize()
+
+    names = ["rvq_assign", "cgr_encode", "cgr_decode", "span_lookup"]
+    evs = [{n: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for n in names}
+           for _ in range(args.steps)]
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for k in range(args.steps):
+        run_step(fkv, cfg, groups, evs[k])
+    stop.record()
+    torch.cuda.synchronize()
+    ms_step = start.elapsed_time(stop) / args.steps
+    phase_ms = {n: float(np.mean([e[n][0].elapsed_time(e[n][1]) for e in evs])) for n in names}
+
+    alg = algorithmic(cfg, groups)
+    tokens = cfg.batch * cfg.T_arch
+    launches = len(groups)
+    rooflines = {}
+    for n in names:
+        t = phase_ms[n] / 1e3 / launches  # average duration of one launch
+        if n == "rvq_assign":
+            ach = alg[n]["flops"] / launches / t / 1e12
+            rooflines[n] = {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_FP16_MFMA_TFLOPS,
+                            "unit": "TFLOP/s", "frac": round(ach / PEAK_FP16_MFMA_TFLOPS, 4)}
+        else:
+            ach = alg[n]["bytes"] / launches / t / 1e9
+            rooflines[n] = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                            "frac": round(ach / PEAK_HBM_GBS, 4)}
+        rooflines[n]["traffic"] = measured_traffic(n, cfg.name)
+        rooflines[n]["avg_launch_us"] = round(t * 1e6, 2)
+    dominant = max(names, key=lambda n: phase_ms[n])
+    roof = dict(rooflines[dominant])
+    roof["kernel"] = dominant
+
+    line = {
+        "metric": METRIC,
+        "value": round(tokens / (ms_step / 1e3), 1),
+        "unit": "archived tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16 (RVQ matrix cores, fp32 accumulate) / f64 (span codec)",
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "description": cfg.description, "layers": cfg.layers,
+                   "heads": cfg.heads, "head_dim": cfg.d, "tokens": cfg.T, "batch": cfg.batch,
+                   "archived_tokens": cfg.T_arch,
+                   "groups": [{"kinds": list(gr["g"].kinds), "S": gr["g"].S, "K": gr["g"].K, "N": gr["g"].N,
+                               "L": gr["codec"].L, "streams": gr["ns"]} for gr in groups],
+                   "lookups_per_step": alg["lookups"]},
+        "phases_ms": {n: round(v, 5) for n, v in phase_ms.items()},
+        "write_tokens_per_s": round(tokens / ((phase_ms["rvq_assign"] + phase_ms["cgr_encode"]) / 1e3), 1),
+        "head_vectors_per_s": round(alg["head_vectors"] / (phase_ms["rvq_assign"] / 1e3), 1),
+        "decoded_symbols_per_s": round(alg["symbols"] / (phase_ms["cgr_decode"] / 1e3), 1),
+        "lookups_per_s": round(alg["lookups"] / (phase_ms["span_lookup"] / 1e3), 1),
+        "roofline": roof,
+        "rooflines": rooflines,
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(cfg, groups, args.cpu_streams)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

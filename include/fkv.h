@@ -1,0 +1,170 @@
+/*
+ * fkv.h -- C ABI of libfkv, the MI355X (gfx950) hot path of the fractal
+ * KV-cache archive (Gusev, "Fractal KV-Cache Archives: Lossless Symbolic
+ * Storage with In-Place Retrieval for Long-Context LLM Inference",
+ * arXiv 2607.07144).
+ *
+ * The archive stores a quantized KV cache as symbol streams (codebook indices
+ * from per-head residual VQ, Sec. 3 "Setup") serialised by a contractive
+ * iterated-map (chaos-game) code on a regular N-gon, one fp64 point per
+ * fixed-length span (Sec. 1 "The code", Sec. 2).  The calls below are the
+ * steps of that path: residual-VQ assignment, span encode, bulk span decode
+ * and O(1) random access.
+ *
+ * Conventions shared by every call:
+ *   - Device pointers are plain device addresses owned by the caller (for
+ *     example PyTorch tensors); the library never allocates, frees or
+ *     synchronises in these calls, and keeps no global mutable state, so
+ *     calls are re-entrant.  `stream` is a hipStream_t (NULL = the null
+ *     stream); all device work is enqueued on it asynchronously.
+ *   - Arguments are validated on the host before anything is enqueued.  An
+ *     invalid call returns a negative fkv_status and has no side effect.
+ *   - Data-dependent outcomes (a span failing its anchor check, an
+ *     out-of-range lookup, an invalid book id) are reported on the device
+ *     only, through the optional per-item status arrays and counters.
+ *     Counters are ACCUMULATED with atomic adds: the caller zeroes them.
+ *   - Symbols are bytes (alphabets of at most 256 letters).  A symbol value
+ *     >= N in an encode input is invalid input: the affected span's point is
+ *     NaN.
+ *   - Layouts are row-major C arrays as written in each comment.
+ */
+#ifndef FKV_H
+#define FKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    FKV_OK = 0,
+    FKV_ERR_INVALID_ARG = -1, /* a null pointer, a size or value out of range, a bad alignment */
+    FKV_ERR_UNSUPPORTED = -2, /* valid by the paper but outside what this build implements */
+    FKV_ERR_LAUNCH = -3,      /* the HIP runtime refused the launch (hipGetLastError) */
+    FKV_ERR_NO_DEVICE = -4    /* no usable gfx950 device is current */
+} fkv_status;
+
+/* Codec parameters of one alphabet (Sec. 1 "The code"; Fig. 1).
+ *   N      alphabet size, 3 <= N <= 256; vertex c of the regular N-gon is at
+ *          angle 2*pi*c/N on the unit circle centred at the origin
+ *   r_max  the packing limit r_N below which the N cells (contracted copies
+ *          of the polygon) are pairwise disjoint, r_N = s/(s+m) with
+ *          s = sin(pi/N), m = max_j sin((2j+1)pi/N); r_3 = r_4 = 1/2
+ *   r      the contraction ratio, r = r_scale * r_N
+ *   L      symbols per stored point: floor(44 / log2(1/r)) (the precision
+ *          budget of one double, Sec. 1), or an explicit override */
+typedef struct {
+    int32_t N;
+    int32_t L;
+    double r;
+    double r_max;
+} fkv_codec;
+
+/* Fills *out for alphabet N.  r_scale in (0, 1]; L_override = 0 selects
+ * floor(44/log2(1/r)), otherwise 1 <= L_override <= 64.  Host only. */
+int fkv_codec_init(int32_t N, double r_scale, int32_t L_override, fkv_codec* out);
+
+/* Size in bytes of the codec's device table (opaque layout, 16-byte aligned
+ * sections: vertex table V(c), cell centres (1-r)V(c) and their 1/r
+ * multiples, and a sector look-up table used by decode). */
+size_t fkv_codec_table_bytes(const fkv_codec* c);
+
+/* Writes the device table into caller host memory of fkv_codec_table_bytes()
+ * bytes.  The caller copies it once to device memory (16-byte aligned) and
+ * passes that copy as `dev_table` below.  Host only. */
+int fkv_codec_fill_table(const fkv_codec* c, void* host_table);
+
+/* ceil(n_sym / L): stored points per stream (the last span may be shorter). */
+int64_t fkv_num_spans(const fkv_codec* c, int64_t n_sym);
+
+/* ---- a2: per-head residual-VQ assignment (Sec. 3 "Setup") ---------------
+ * For every stream s and archived token t in [t_begin, t_end), starting from
+ * r = x[s][t] and for stage st = 0..S-1:
+ *     i_st = argmin_j ||r - C[b][st][j]||^2   (lowest j on exact ties)
+ *     r    = r - C[b][st][i_st]
+ * with b = stream_book[s].  The S indices sum (through their centroids) to
+ * the reconstruction of the vector.
+ *   desc.n_streams, desc.T   x is [n_streams][T][d] IEEE binary16
+ *   desc.t_begin, t_end      archived token range (exact-window policy:
+ *                            first 4 sinks and last 32 recent stay exact)
+ *   desc.d                   head dim, multiple of 16, 16..256
+ *   desc.S, desc.K           stages (1..8) and codewords per stage (1..256)
+ *   desc.n_books             books is [n_books][S][K][d] binary16
+ *   stream_book              device int32 [n_streams]; an id outside
+ *                            [0, n_books) marks the stream invalid: its
+ *                            symbols are set to 0xFF and *n_bad_streams (if
+ *                            given) is incremented
+ *   symbols                  device out u8 [n_streams][(t_end-t_begin)*S],
+ *                            token-major, stage-minor
+ *   residual                 device out f32 [n_streams][t_end-t_begin][d],
+ *                            x - sum_st C[b][st][i_st]; nullable
+ * Distances are evaluated as ||c||^2/2 - r.c with fp16 operands on matrix
+ * cores and fp32 accumulation; residuals beyond the first stage are split
+ * into two fp16 parts so both products stay exact.  x, books: 16-byte
+ * aligned. */
+typedef struct {
+    int64_t n_streams;
+    int64_t T;
+    int64_t t_begin;
+    int64_t t_end;
+    int32_t d;
+    int32_t S;
+    int32_t K;
+    int32_t n_books;
+} fkv_rvq_desc;
+
+int fkv_rvq_assign(const fkv_rvq_desc* desc, const uint16_t* x_f16, const uint16_t* books_f16,
+                   const int32_t* stream_book, uint8_t* symbols, float* residual,
+                   uint32_t* n_bad_streams, void* stream);
+
+/* ---- a3: fixed-span chaos-game encode (Sec. 1 "The code", Sec. 2) --------
+ * symbols [n_streams][n_sym] (device u8) -> points [n_streams][n_spans][2]
+ * (device f64, x then y; 16-byte aligned), n_spans = fkv_num_spans().
+ * Span j covers symbols [jL, min((j+1)L, n_sym)) and is encoded from the
+ * anchor (0,0) by p = V(c) + r (p - V(c)), each coordinate evaluated as
+ * t = p - V; u = r*t; p = V + u with round-to-nearest-even and no fused
+ * multiply-add, so points are bit-for-bit reproducible. */
+int fkv_cgr_encode_spans(const fkv_codec* c, const void* dev_table, const uint8_t* symbols,
+                         int64_t n_streams, int64_t n_sym, double* points, void* stream);
+
+/* ---- a4: bulk span decode (Sec. 1 "The code") ----------------------------
+ * points [n_streams][n_spans][2] -> symbols [n_streams][n_sym].  Each span
+ * is walked backward from its stored point: the symbol is the cell holding
+ * the point (nearest cell centre (1-r)V(c), equivalently the angular
+ * sector), then p <- (p - (1-r)V(c)) / r.  Anchored reconstruction: after
+ * the span's steps the point must be back at the anchor (0,0); a span is
+ * accepted when max(|x|,|y|) <= 2^-6 and, with verify != 0, when re-encoding
+ * its decoded symbols reproduces the stored point bit for bit.
+ *   span_ok   device out u8 [n_streams][n_spans] (1 accepted, 0 failed); nullable
+ *   n_failed  device u32 counter, += number of failed spans; nullable
+ * Symbols of a failed span are unspecified (but always < N). */
+int fkv_cgr_decode_spans(const fkv_codec* c, const void* dev_table, const double* points,
+                         int64_t n_streams, int64_t n_sym, uint8_t* symbols, uint8_t* span_ok,
+                         uint32_t* n_failed, int32_t verify, void* stream);
+
+/* ---- a5: O(1) random access (Sec. 2, Table 1 "random access") -------------
+ * For query q with (s, t) = (q_stream[q], q_token[q]): a = t*S; decode only
+ * the span(s) holding symbols [a, a+S) of stream s and write them to
+ * out[q][0..S).  n_sym must be a multiple of S (S symbols per token).
+ *   q_status  device out u8 [n_q]: 0 ok, 1 a decoded span failed its anchor
+ *             check, 2 out of range (s >= n_streams or t >= n_sym/S; out
+ *             row left zero); nullable
+ *   n_failed  device u32 counter, += number of queries with status != 0; nullable */
+int fkv_span_lookup(const fkv_codec* c, const void* dev_table, const double* points,
+                    int64_t n_streams, int64_t n_sym, int32_t S, const uint32_t* q_stream,
+                    const uint32_t* q_token, int64_t n_q, uint8_t* out, uint8_t* q_status,
+                    uint32_t* n_failed, void* stream);
+
+/* Static description of a status code. */
+const char* fkv_status_string(int status);
+
+/* Library version string. */
+const char* fkv_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FKV_H */

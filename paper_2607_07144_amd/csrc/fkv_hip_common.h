@@ -1,0 +1,72 @@
+// fkv_hip_common.h -- small device/host helpers shared by libfkv's kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "fkv.h"
+
+namespace fkv {
+
+// Maps the last HIP error of this thread to a status code.
+inline int launch_status()
+{
+    hipError_t e = hipGetLastError();
+    if (e == hipSuccess) return FKV_OK;
+    if (e == hipErrorNoDevice || e == hipErrorInvalidDevice) return FKV_ERR_NO_DEVICE;
+    return FKV_ERR_LAUNCH;
+}
+
+inline bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
+
+// Copies global bytes [g0, g1) of `src` into LDS so that global byte g sits at
+// LDS byte (g - (g0 & ~3)).  Whole aligned dwords are moved as dwords; the
+// partial dwords at either end byte by byte, so nothing outside [g0, g1) is
+// touched.  `src` must be 4-byte aligned.  Block-cooperative, no barrier.
+__device__ inline void bytes_to_lds(const uint8_t* __restrict__ src, int64_t g0, int64_t g1,
+                                    uint8_t* lds)
+{
+    const int tid = threadIdx.x, nt = blockDim.x;
+    const int64_t base = g0 & ~(int64_t)3;
+    const int64_t a0 = (g0 + 3) & ~(int64_t)3;
+    const int64_t a1 = g1 & ~(int64_t)3;
+    if (a0 >= a1) {
+        for (int64_t g = g0 + tid; g < g1; g += nt) lds[g - base] = src[g];
+        return;
+    }
+    const uint32_t* s32 = (const uint32_t*)src;
+    uint32_t* l32 = (uint32_t*)(lds + (a0 - base));
+    for (int64_t w = (a0 >> 2) + tid; w < (a1 >> 2); w += nt) l32[w - (a0 >> 2)] = s32[w];
+    if (tid < a0 - g0) lds[g0 + tid - base] = src[g0 + tid];
+    if (tid < g1 - a1) lds[a1 + tid - base] = src[a1 + tid];
+}
+
+// Inverse of bytes_to_lds: writes LDS bytes back to global [g0, g1).
+__device__ inline void lds_to_bytes(const uint8_t* lds, int64_t g0, int64_t g1,
+                                    uint8_t* __restrict__ dst)
+{
+    const int tid = threadIdx.x, nt = blockDim.x;
+    const int64_t base = g0 & ~(int64_t)3;
+    const int64_t a0 = (g0 + 3) & ~(int64_t)3;
+    const int64_t a1 = g1 & ~(int64_t)3;
+    if (a0 >= a1) {
+        for (int64_t g = g0 + tid; g < g1; g += nt) dst[g] = lds[g - base];
+        return;
+    }
+    uint32_t* d32 = (uint32_t*)dst;
+    const uint32_t* l32 = (const uint32_t*)(lds + (a0 - base));
+    for (int64_t w = (a0 >> 2) + tid; w < (a1 >> 2); w += nt) d32[w] = l32[w - (a0 >> 2)];
+    if (tid < a0 - g0) dst[g0 + tid] = lds[g0 + tid - base];
+    if (tid < g1 - a1) dst[a1 + tid] = lds[a1 + tid - base];
+}
+
+// Adds the number of lanes of the block with `flag` set to *counter, one
+// atomic per wave that has any.
+__device__ inline void count_flags(bool flag, uint32_t* counter)
+{
+    if (!counter) return;
+    const unsigned long long m = __ballot(flag);
+    if (m && (threadIdx.x & 63) == 0) atomicAdd(counter, (uint32_t)__popcll(m));
+}
+
+}  // namespace fkv

@@ -1,0 +1,228 @@
+"""ctypes binding of libfkv (include/fkv.h), with the C names.
+
+Argument marshalling only: every step of the archive path runs in the HIP
+kernels of libfkv.so.  PyTorch provides device memory and the current HIP
+stream.  Importing this module loads the library and raises ImportError when
+it has not been built -- there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libfkv.so")
+if not os.path.exists(_LIB_PATH):
+    raise ImportError("libfkv.so is not built (run paper_2607_07144_amd.build.build() or "
+                      "__graft_entry__.build()); there is no fallback implementation")
+lib = ctypes.CDLL(_LIB_PATH)
+
+FKV_OK = 0
+FKV_ERR_INVALID_ARG = -1
+FKV_ERR_UNSUPPORTED = -2
+FKV_ERR_LAUNCH = -3
+FKV_ERR_NO_DEVICE = -4
+
+
+class fkv_codec(ctypes.Structure):
+    _fields_ = [("N", ctypes.c_int32), ("L", ctypes.c_int32), ("r", ctypes.c_double),
+                ("r_max", ctypes.c_double)]
+
+
+class fkv_rvq_desc(ctypes.Structure):
+    _fields_ = [("n_streams", ctypes.c_int64), ("T", ctypes.c_int64), ("t_begin", ctypes.c_int64),
+                ("t_end", ctypes.c_int64), ("d", ctypes.c_int32), ("S", ctypes.c_int32),
+                ("K", ctypes.c_int32), ("n_books", ctypes.c_int32)]
+
+
+_i32, _i64, _dbl, _p, _sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_double, ctypes.c_void_p, ctypes.c_size_t
+_PC = ctypes.POINTER(fkv_codec)
+_SIGS = {
+    "fkv_codec_init": ([_i32, _dbl, _i32, _PC], ctypes.c_int),
+    "fkv_codec_table_bytes": ([_PC], _sz),
+    "fkv_codec_fill_table": ([_PC, _p], ctypes.c_int),
+    "fkv_num_spans": ([_PC, _i64], _i64),
+    "fkv_rvq_assign": ([ctypes.POINTER(fkv_rvq_desc), _p, _p, _p, _p, _p, _p, _p], ctypes.c_int),
+    "fkv_cgr_encode_spans": ([_PC, _p, _p, _i64, _i64, _p, _p], ctypes.c_int),
+    "fkv_cgr_decode_spans": ([_PC, _p, _p, _i64, _i64, _p, _p, _p, _i32, _p], ctypes.c_int),
+    "fkv_span_lookup": ([_PC, _p, _p, _i64, _i64, _i32, _p, _p, _i64, _p, _p, _p, _p], ctypes.c_int),
+    "fkv_status_string": ([ctypes.c_int], ctypes.c_char_p),
+    "fkv_version": ([], ctypes.c_char_p),
+}
+for _name, (_args, _res) in _SIGS.items():
+    _f = getattr(lib, _name)
+    _f.argtypes = _args
+    _f.restype = _res
+
+
+class FkvError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__("%s: %s (%d)" % (where, lib.fkv_status_string(status).decode(), status))
+        self.status = status
+
+
+def _check(status: int, where: str) -> None:
+    if status != FKV_OK:
+        raise FkvError(status, where)
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is not None:
+        return ctypes.c_void_p(int(stream))
+    return ctypes.c_void_p(_torch().cuda.current_stream().cuda_stream)
+
+
+def _need(t, dtype, name):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor) or not t.is_cuda or t.dtype != dtype or not t.is_contiguous():
+        raise TypeError("%s must be a contiguous CUDA tensor of %s" % (name, dtype))
+
+
+# ------------------------------------------------------------------ codec
+
+class Codec:
+    """Host codec parameters (a fkv_codec) plus the device table built from them."""
+
+    def __init__(self, N: int, r_scale: float = 0.98, L_override: int = 0):
+        self.c = fkv_codec()
+        _check(lib.fkv_codec_init(N, r_scale, L_override, ctypes.byref(self.c)), "fkv_codec_init")
+        self._table = None
+
+    N = property(lambda self: self.c.N)
+    L = property(lambda self: self.c.L)
+    r = property(lambda self: self.c.r)
+    r_max = property(lambda self: self.c.r_max)
+
+    def n_spans(self, n_sym: int) -> int:
+        return int(lib.fkv_num_spans(ctypes.byref(self.c), n_sym))
+
+    def host_table(self) -> np.ndarray:
+        n = lib.fkv_codec_table_bytes(ctypes.byref(self.c))
+        buf = np.zeros(n, np.uint8)
+        _check(lib.fkv_codec_fill_table(ctypes.byref(self.c), buf.ctypes.data), "fkv_codec_fill_table")
+        return buf
+
+    def table(self, device="cuda"):
+        """The device copy of the table (built once per Codec)."""
+        if self._table is None:
+            torch = _torch()
+            self._table = torch.from_numpy(self.host_table()).to(device)
+        return self._table
+
+
+def fkv_codec_init(N: int, r_scale: float = 0.98, L_override: int = 0) -> Codec:
+    return Codec(N, r_scale, L_override)
+
+
+# ------------------------------------------------------------------ a2: residual VQ
+
+def fkv_rvq_assign(x, books, stream_book, t_begin: int, t_end: int, symbols=None, residual=None,
+                   want_residual: bool = False, n_bad=None, stream=None):
+    """x f16 [n_streams][T][d], books f16 [n_books][S][K][d], stream_book i32 [n_streams] (all CUDA).
+    Returns (symbols u8 [n_streams][(t_end-t_begin)*S], residual f32 or None)."""
+    torch = _torch()
+    _need(x, torch.float16, "x")
+    _need(books, torch.float16, "books")
+    _need(stream_book, torch.int32, "stream_book")
+    ns, T, d = x.shape
+    nb, S, K, d2 = books.shape
+    if d2 != d or stream_book.shape != (ns,):
+        raise ValueError("shape mismatch between x, books and stream_book")
+    Ta = t_end - t_begin
+    if symbols is None:
+        symbols = torch.empty((ns, Ta * S), dtype=torch.uint8, device=x.device)
+    _need(symbols, torch.uint8, "symbols")
+    if symbols.numel() != ns * Ta * S:
+        raise ValueError("symbols has the wrong size")
+    if residual is None and want_residual:
+        residual = torch.empty((ns, Ta, d), dtype=torch.float32, device=x.device)
+    if residual is not None:
+        _need(residual, torch.float32, "residual")
+        if residual.numel() != ns * Ta * d:
+            raise ValueError("residual has the wrong size")
+    if n_bad is not None:
+        _need(n_bad, torch.int32, "n_bad")
+    desc = fkv_rvq_desc(ns, T, t_begin, t_end, d, S, K, nb)
+    _check(lib.fkv_rvq_assign(ctypes.byref(desc), _ptr(x), _ptr(books), _ptr(stream_book), _ptr(symbols),
+                              _ptr(residual), _ptr(n_bad), _stream(stream)), "fkv_rvq_assign")
+    return symbols, residual
+
+
+# ------------------------------------------------------------------ a3: encode
+
+def fkv_cgr_encode_spans(codec: Codec, symbols, points=None, stream=None):
+    """symbols u8 [n_streams][n_sym] -> points f64 [n_streams][n_spans][2]."""
+    torch = _torch()
+    _need(symbols, torch.uint8, "symbols")
+    ns, n_sym = symbols.shape
+    if points is None:
+        points = torch.empty((ns, codec.n_spans(n_sym), 2), dtype=torch.float64, device=symbols.device)
+    _need(points, torch.float64, "points")
+    if points.numel() != ns * codec.n_spans(n_sym) * 2:
+        raise ValueError("points has the wrong size")
+    _check(lib.fkv_cgr_encode_spans(ctypes.byref(codec.c), _ptr(codec.table(symbols.device)), _ptr(symbols),
+                                    ns, n_sym, _ptr(points), _stream(stream)), "fkv_cgr_encode_spans")
+    return points
+
+
+# ------------------------------------------------------------------ a4: decode
+
+def fkv_cgr_decode_spans(codec: Codec, points, n_sym: int, symbols=None, span_ok=None, n_failed=None,
+                         verify: bool = False, stream=None):
+    """points f64 [n_streams][n_spans][2] -> symbols u8 [n_streams][n_sym] (span_ok, n_failed optional)."""
+    torch = _torch()
+    _need(points, torch.float64, "points")
+    ns = points.shape[0]
+    if points.numel() != ns * codec.n_spans(n_sym) * 2:
+        raise ValueError("points does not match n_sym")
+    if symbols is None:
+        symbols = torch.empty((ns, n_sym), dtype=torch.uint8, device=points.device)
+    _need(symbols, torch.uint8, "symbols")
+    if span_ok is not None:
+        _need(span_ok, torch.uint8, "span_ok")
+    if n_failed is not None:
+        _need(n_failed, torch.int32, "n_failed")
+    _check(lib.fkv_cgr_decode_spans(ctypes.byref(codec.c), _ptr(codec.table(points.device)), _ptr(points),
+                                    ns, n_sym, _ptr(symbols), _ptr(span_ok), _ptr(n_failed),
+                                    1 if verify else 0, _stream(stream)), "fkv_cgr_decode_spans")
+    return symbols
+
+
+# ------------------------------------------------------------------ a5: lookup
+
+def fkv_span_lookup(codec: Codec, points, n_sym: int, S: int, q_stream, q_token, out=None, q_status=None,
+                    n_failed=None, stream=None):
+    """Random access: out u8 [n_q][S] with the S symbols of each (stream, token) query."""
+    torch = _torch()
+    _need(points, torch.float64, "points")
+    _need(q_stream, torch.int32, "q_stream")
+    _need(q_token, torch.int32, "q_token")
+    nq = q_stream.numel()
+    if q_token.numel() != nq:
+        raise ValueError("q_stream and q_token differ in length")
+    if out is None:
+        out = torch.empty((nq, S), dtype=torch.uint8, device=points.device)
+    _need(out, torch.uint8, "out")
+    if q_status is not None:
+        _need(q_status, torch.uint8, "q_status")
+    if n_failed is not None:
+        _need(n_failed, torch.int32, "n_failed")
+    ns = points.shape[0]
+    _check(lib.fkv_span_lookup(ctypes.byref(codec.c), _ptr(codec.table(points.device)), _ptr(points), ns,
+                               n_sym, S, _ptr(q_stream), _ptr(q_token), nq, _ptr(out), _ptr(q_status),
+                               _ptr(n_failed), _stream(stream)), "fkv_span_lookup")
+    return out
+
+
+def fkv_version() -> str:
+    return lib.fkv_version().decode()

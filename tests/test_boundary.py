@@ -1,0 +1,160 @@
+"""CPU tests of the C-ABI boundary: the library loads, exports every declared
+symbol, rejects invalid arguments before touching a device, and its host-side
+codec setup agrees bit for bit with the oracle's independent computation."""
+import ctypes
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fkv.h")
+
+
+@pytest.fixture(scope="module")
+def F():
+    from paper_2607_07144_amd import fkv
+    return fkv
+
+
+def declared_functions():
+    txt = open(HEADER).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(fkv_[a-z_0-9]+)\s*\(", txt)))
+
+
+def test_library_exports_every_declared_function(F):
+    names = declared_functions()
+    assert len(names) >= 10
+    for n in names:
+        assert hasattr(F.lib, n), n
+    assert F.fkv_version().startswith("fkv")
+    for s in (0, -1, -2, -3, -4, 7):
+        assert F.lib.fkv_status_string(s)
+
+
+def test_codec_matches_oracle_bit_for_bit(F, orc):
+    for N in list(range(3, 33)) + [48, 64, 100, 128, 200, 255, 256]:
+        for scale in (0.5, 0.9, 0.98, 1.0):
+            c = F.Codec(N, scale)
+            o = orc.Codec(N, scale)
+            assert c.r_max == o.r_max and c.r == o.r and c.L == o.L, (N, scale)
+            tab = c.host_table()
+            V = tab[:16 * N].view(np.float64).reshape(N, 2)
+            W = tab[16 * N:32 * N].view(np.float64).reshape(N, 2)
+            assert np.array_equal(V, o.V) and np.array_equal(W, o.W), (N, scale)
+    c = F.Codec(256, 0.98, 9)
+    assert c.L == 9 and c.n_spans(100) == 12 and c.n_spans(0) == 0
+
+
+def _sector_fast_emulated(tab, N, q):
+    """NumPy emulation of the kernel's look-up-table sector search (fp32 pseudo-angle)."""
+    lut = tab[48 * N:].view(np.dtype([("thr", "<f4"), ("lo", "<u2"), ("hi", "<u2")]))
+    fx = q[:, 0].astype(np.float32)
+    fy = q[:, 1].astype(np.float32)
+    s = np.abs(fx) + np.abs(fy)
+    d = fy / s
+    P = np.where(fx >= 0, d, np.float32(2) - d).astype(np.float32)
+    P = np.clip(P, -1, 2.99999).astype(np.float32)
+    idx = np.minimum(((P + 1) * 128).astype(np.int32), 511)
+    e = lut[idx]
+    return np.where(P >= e["thr"], e["hi"], e["lo"]).astype(np.int64)
+
+
+@pytest.mark.parametrize("N", [3, 4, 5, 7, 16, 17, 64, 100, 256])
+def test_sector_table_agrees_with_oracle_cells(F, orc, N):
+    """The decode look-up table picks the oracle's nearest cell centre for every point whose
+    margin from the sector lines is certified (points of valid spans), here sampled densely."""
+    c = F.Codec(N, 0.98)
+    o = orc.Codec(N, 0.98)
+    tab = c.host_table()
+    rng = np.random.default_rng(N)
+    # valid points: stored points of random spans and every intermediate of their backward walk
+    L = c.L
+    sym = rng.integers(0, N, size=(1, 4000 * L), dtype=np.uint8)
+    cc = orc.Codec(N, 0.98, L_override=L)
+    pts = orc.encode(cc, sym)[0]
+    q = pts.copy()
+    for k in range(L - 1, -1, -1):
+        got = _sector_fast_emulated(tab, N, q)
+        want = sym[0].reshape(-1, L)[:, k]
+        assert np.array_equal(got, want), (N, k)
+        q = (q - o.W[want]) / o.r
+    # plus random points anywhere in the unit disk away from the sector lines
+    q = rng.uniform(-1, 1, size=(20000, 2))
+    ang = np.arctan2(q[:, 1], q[:, 0])
+    frac = (ang * N / (2 * np.pi)) % 1.0
+    keep = (np.abs(frac - 0.5) > 1e-4 * N) & (np.hypot(q[:, 0], q[:, 1]) > 1e-3)
+    q = q[keep]
+    got = _sector_fast_emulated(tab, N, q)
+    want = np.array([orc.cell(o, a, b) for a, b in q])
+    assert np.array_equal(got, want)
+
+
+def test_invalid_arguments_are_rejected_on_the_host(F):
+    lib = F.lib
+    E = F.FKV_ERR_INVALID_ARG
+    c = F.fkv_codec()
+    assert lib.fkv_codec_init(2, 0.98, 0, ctypes.byref(c)) == E
+    assert lib.fkv_codec_init(257, 0.98, 0, ctypes.byref(c)) == E
+    assert lib.fkv_codec_init(16, 0.0, 0, ctypes.byref(c)) == E
+    assert lib.fkv_codec_init(16, 1.01, 0, ctypes.byref(c)) == E
+    assert lib.fkv_codec_init(16, float("nan"), 0, ctypes.byref(c)) == E
+    assert lib.fkv_codec_init(16, 0.98, 65, ctypes.byref(c)) == E
+    assert lib.fkv_codec_init(16, 0.98, -1, ctypes.byref(c)) == E
+    assert lib.fkv_codec_init(16, 0.98, 0, None) == E
+    assert lib.fkv_codec_init(16, 0.98, 0, ctypes.byref(c)) == 0
+    assert lib.fkv_codec_fill_table(ctypes.byref(c), None) == E
+    assert lib.fkv_num_spans(None, 5) == -1
+    P = ctypes.c_void_p
+    good16, odd = P(0x10000), P(0x10001)
+    # encode / decode / lookup: bad codec, nulls, misalignment, bad flags
+    bad = F.fkv_codec(16, 0, 0.1, 0.2)
+    assert lib.fkv_cgr_encode_spans(ctypes.byref(bad), good16, good16, 1, 10, good16, None) == E
+    assert lib.fkv_cgr_encode_spans(ctypes.byref(c), None, good16, 1, 10, good16, None) == E
+    assert lib.fkv_cgr_encode_spans(ctypes.byref(c), good16, None, 1, 10, good16, None) == E
+    assert lib.fkv_cgr_encode_spans(ctypes.byref(c), good16, odd, 1, 10, good16, None) == E
+    assert lib.fkv_cgr_encode_spans(ctypes.byref(c), good16, good16, 1, 10, P(0x10008), None) == E
+    assert lib.fkv_cgr_encode_spans(ctypes.byref(c), good16, good16, -1, 10, good16, None) == E
+    assert lib.fkv_cgr_decode_spans(ctypes.byref(c), good16, good16, 1, 10, good16, None, None, 2, None) == E
+    assert lib.fkv_cgr_decode_spans(ctypes.byref(c), good16, P(0x10008), 1, 10, good16, None, None, 0,
+                                    None) == E
+    assert lib.fkv_cgr_decode_spans(ctypes.byref(c), good16, good16, 1, 10, good16, None, odd, 0, None) == E
+    assert lib.fkv_span_lookup(ctypes.byref(c), good16, good16, 1, 10, 3, good16, good16, 5, good16, None,
+                               None, None) == E   # n_sym not a multiple of S
+    assert lib.fkv_span_lookup(ctypes.byref(c), good16, good16, 1, 10, 9, good16, good16, 5, good16, None,
+                               None, None) == E   # S > 8
+    assert lib.fkv_span_lookup(ctypes.byref(c), good16, good16, 1, 10, 2, None, good16, 5, good16, None,
+                               None, None) == E
+    assert lib.fkv_span_lookup(ctypes.byref(c), good16, good16, 1, 10, 2, good16, odd, 5, good16, None,
+                               None, None) == E
+    # empty work is a no-op that never reaches the device
+    assert lib.fkv_cgr_encode_spans(ctypes.byref(c), good16, None, 0, 10, None, None) == 0
+    assert lib.fkv_cgr_decode_spans(ctypes.byref(c), good16, None, 3, 0, None, None, None, 0, None) == 0
+    assert lib.fkv_span_lookup(ctypes.byref(c), good16, None, 0, 0, 2, None, None, 0, None, None, None,
+                               None) == 0
+    # residual VQ descriptor checks
+    D = F.fkv_rvq_desc
+
+    def rvq(desc, x=good16, b=good16, sb=good16, sym=good16, res=None, nbad=None):
+        return lib.fkv_rvq_assign(ctypes.byref(desc) if desc is not None else None, x, b, sb, sym, res,
+                                  nbad, None)
+
+    assert rvq(None) == E
+    assert rvq(D(4, 100, 4, 101, 64, 2, 256, 4)) == E   # t_end > T
+    assert rvq(D(4, 100, 50, 40, 64, 2, 256, 4)) == E   # t_end < t_begin
+    assert rvq(D(4, 100, 4, 68, 72, 2, 256, 4)) == E    # d not a multiple of 16
+    assert rvq(D(4, 100, 4, 68, 272, 2, 256, 4)) == E   # d > 256
+    assert rvq(D(4, 100, 4, 68, 64, 0, 256, 4)) == E    # S = 0
+    assert rvq(D(4, 100, 4, 68, 64, 9, 256, 4)) == E    # S > 8
+    assert rvq(D(4, 100, 4, 68, 64, 2, 257, 4)) == E    # K > 256
+    assert rvq(D(4, 100, 4, 68, 64, 2, 0, 4)) == E      # K = 0
+    assert rvq(D(4, 100, 4, 68, 64, 2, 256, 0)) == E    # no books
+    assert rvq(D(4, 100, 4, 68, 64, 2, 256, 4), x=None) == E
+    assert rvq(D(4, 100, 4, 68, 64, 2, 256, 4), x=P(0x10008)) == E
+    assert rvq(D(4, 100, 4, 68, 64, 2, 256, 4), sb=odd) == E
+    assert rvq(D(4, 100, 4, 68, 64, 2, 256, 4), res=P(0x10004)) == E
+    assert rvq(D(0, 100, 4, 68, 64, 2, 256, 4), x=None, b=None, sb=None, sym=None) == 0
+    assert rvq(D(4, 100, 10, 10, 64, 2, 256, 4), x=None, b=None, sb=None, sym=None) == 0
