@@ -9,7 +9,9 @@ O(1) lookups.  Inputs are resident in device memory before the timed region.
 Prints one JSON line.  `value` is archived tokens per second over the whole
 step (a token is one position across all layers, heads and K/V); per-phase
 rates, the dominant kernel's roofline fraction and the CPU oracle's rate on the
-same workload are reported beside it.
+same workload are reported beside it.  The step is captured once as a HIP graph
+and replayed (no host launch overhead in the timed region); each kernel's
+average duration comes from a graph of back-to-back launches of that kernel.
 """
 from __future__ import annotations
 
@@ -94,25 +96,25 @@ def build_workload(name: str, n_lookups: int):
     return cfg, groups
 
 
-def run_step(fkv, cfg, groups, ev=None):
+def run_kernel(fkv, cfg, groups, name):
+    """One launch of one step kernel for every group, on the current stream."""
     for gr in groups:
-        if ev is not None:
-            ev["rvq_assign"][0].record()
-        fkv.fkv_rvq_assign(gr["x"], gr["books"], gr["sb"], cfg.t_begin, cfg.t_end, symbols=gr["sym"])
-        if ev is not None:
-            ev["rvq_assign"][1].record()
-            ev["cgr_encode"][0].record()
-        fkv.fkv_cgr_encode_spans(gr["codec"], gr["sym"], points=gr["pts"])
-        if ev is not None:
-            ev["cgr_encode"][1].record()
-            ev["cgr_decode"][0].record()
-        fkv.fkv_cgr_decode_spans(gr["codec"], gr["pts"], gr["n_sym"], symbols=gr["dec"])
-        if ev is not None:
-            ev["cgr_decode"][1].record()
-            ev["span_lookup"][0].record()
-        fkv.fkv_span_lookup(gr["codec"], gr["pts"], gr["n_sym"], gr["g"].S, gr["qs"], gr["qt"], out=gr["out"])
-        if ev is not None:
-            ev["span_lookup"][1].record()
+        if name == "rvq_assign":
+            fkv.fkv_rvq_assign(gr["x"], gr["books"], gr["sb"], cfg.t_begin, cfg.t_end, symbols=gr["sym"])
+        elif name == "cgr_encode":
+            fkv.fkv_cgr_encode_spans(gr["codec"], gr["sym"], points=gr["pts"])
+        elif name == "cgr_decode":
+            fkv.fkv_cgr_decode_spans(gr["codec"], gr["pts"], gr["n_sym"], symbols=gr["dec"])
+        else:
+            fkv.fkv_span_lookup(gr["codec"], gr["pts"], gr["n_sym"], gr["g"].S, gr["qs"], gr["qt"],
+                                out=gr["out"])
+
+
+def run_step(fkv, cfg, groups):
+    """One pass of the whole path: assign, encode, decode, look up (per group)."""
+    for gr in groups:
+        for name in ("rvq_assign", "cgr_encode", "cgr_decode", "span_lookup"):
+            run_kernel(fkv, cfg, [gr], name)
 
 
 def algorithmic(cfg, groups):
@@ -188,23 +190,47 @@ def main():
 
     torch.cuda.set_device(0)
     cfg, groups = build_workload(args.workload, args.lookups)
-    torch.cuda.synchronize()
-    for _ in range(args.warmup):
-        run_step(fkv, cfg, groups)
+    names = ["rvq_assign", "cgr_encode", "cgr_decode", "span_lookup"]
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        for _ in range(max(1, args.warmup)):
+            run_step(fkv, cfg, groups)
     torch.cuda.synchronize()
 
-    names = ["rvq_assign", "cgr_encode", "cgr_decode", "span_lookup"]
-    evs = [{n: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for n in names}
-           for _ in range(args.steps)]
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # The step is captured once as a HIP graph (the four launches of each group)
+    # and replayed, so host launch overhead stays out of the timed region.
+    step_graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(step_graph, stream=side):
+        run_step(fkv, cfg, groups)
+    for _ in range(args.warmup):
+        step_graph.replay()
     torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     start.record()
-    for k in range(args.steps):
-        run_step(fkv, cfg, groups, evs[k])
+    for _ in range(args.steps):
+        step_graph.replay()
     stop.record()
     torch.cuda.synchronize()
     ms_step = start.elapsed_time(stop) / args.steps
-    phase_ms = {n: float(np.mean([e[n][0].elapsed_time(e[n][1]) for e in evs])) for n in names}
+
+    # Average duration of each kernel: a graph of `reps` back-to-back launches of
+    # that kernel alone, replayed and bracketed by events on the launch stream.
+    reps = 10
+    phase_ms = {}
+    for n in names:
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=side):
+            for _ in range(reps):
+                run_kernel(fkv, cfg, groups, n)
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()  # replay() launches on the current stream
+        for _ in range(max(1, args.steps // 4)):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        phase_ms[n] = e0.elapsed_time(e1) / (reps * max(1, args.steps // 4))
 
     alg = algorithmic(cfg, groups)
     tokens = cfg.batch * cfg.T_arch

@@ -22,7 +22,7 @@ SOURCES = ["fkv_codec.cpp", "cgr_kernels.hip", "rvq_kernels.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-COMMON = ["-O3", "-fPIC", "-std=c++17", "-ffp-contract=off", "-fno-fast-math",
+COMMON = ["-O3", "-fPIC", "-std=c++17", "-ffp-contract=off", "-fno-fast-math", "-fno-slp-vectorize",
           "-I" + INCLUDE, "-I" + CSRC]
 # Device code: no packed-fp32 instructions; hipcc's host pass warns that it
 # does not know the feature, which is harmless.

@@ -3,25 +3,42 @@
 //
 // Method (Sec. 3 "Setup" of the paper): an archived K or V head vector x is
 // stored as S codebook indices whose centroids sum to its reconstruction.
-// Greedy residual VQ: r = x; for each stage st, i_st = argmin_j ||r - C_st[j]||^2
-// (lowest j on exact ties), then r -= C_st[i_st].
+// Greedy residual VQ: r_0 = x; for stage s, i_s = argmin_j ||r_s - C_s[j]||^2
+// (lowest j on exact ties), then r_{s+1} = r_s - C_s[i_s].
 //
-// Formulation.  argmin_j ||r - c_j||^2 = argmin_j (||c_j||^2/2 - r.c_j): a dense
-// contraction of the token block against the stage's codebook, plus a per-
-// codeword bias.  The contraction runs on v_mfma_f32_32x32x16_f16 with the
-// codebook as the A operand (32 codewords x 16 dims per instruction, staged in
-// LDS with a 16-byte row pad so the 32 rows of a fragment hit distinct banks)
-// and 32 tokens as the B operand (held in registers for all stages).  The
-// accumulator is seeded with ||c||^2/2, so the finished tile already holds the
-// scores.  In the 32x32 accumulator layout lane l owns token l%32 and 16 of
-// the 32 codewords of the tile, so the argmin is an in-lane scan followed by
-// one exchange with lane l^32.
+// Formulation.  For a token with residual r and stage codebook C:
+//     u_j = r.c_j - ||c_j||^2/2 - b  =  -||r - c_j||^2/2 - (b - ||r||^2/2),
+// with a per-token bias b >= ||r||^2/2, so every u_j is a negative float whose
+// magnitude orders like the squared distance.  All of u_j comes out of the
+// matrix cores (v_mfma_f32_32x32x16_f16, codebook = A operand from LDS,
+// 32 tokens = B operand in registers):
+//   * one "bias step" per 32x32 tile: A row i = (-||c_i||^2/2 split exactly
+//     into three fp16 parts, 1, 2^14), B column j = (1, 1, 1, b_j parts), so
+//     the tile starts at -||c_i||^2/2 - b_j.  b only has to be an upper bound
+//     of ||r||^2/2 (it shifts every score of a token equally), so it is
+//     rounded up into fp16 freely;
+//   * the d/16 data steps add r.c_i.
+// In the 32x32 accumulator layout lane l owns token l%32 and 16 of the tile's
+// 32 codewords, so the argmin is in-lane: a negative float's bits, read as an
+// unsigned integer, grow with its magnitude; with the low 4 bits replaced by
+// the codeword's position among the lane's 16 they form a key whose minimum
+// (v_min3_u32) is the nearest codeword and carries its index.  Dropping 4
+// mantissa bits coarsens the comparison to 2^-19 relative, well inside the
+// 1e-5 near-tie band.  Tiles merge on the value bits (earlier tile wins ties),
+// then lane l with lane l^32.  Stage s's bias is the winning |u| of stage s-1
+// (||r_s||^2/2 plus the previous margin), grown by 2^-10.
 //
-// Precision.  Stage 0 multiplies fp16 x by fp16 codewords: every product is
-// exact in fp32.  From stage 1 on the residual is an fp32 value; it is split
-// as r = hi + lo with hi = fp16(r), lo = fp16(r - hi), and both halves go
-// through the matrix cores into the same accumulator, so the scores keep
-// about 22 bits of the residual instead of fp16's 11.
+// Exact operands.  Stage 0 multiplies fp16 x by fp16 codewords (every product
+// exact in fp32).  Stage 1 uses r_1 = x - c_0 as two fp16 passes, x.c and
+// (-c_0).c, both exact.  From stage 2 on the residual is carried as an fp16
+// pair hi + lo (about 22 bits, rebuilt in fp32 and split again after every
+// stage) and both halves go through the matrix cores.
+//
+// Codebooks.  Each stage's codebook is copied global -> LDS with the
+// asynchronous global_load_lds_dwordx4 into two alternating buffers, so the
+// next stage's book streams in while the current one is in use.  LDS rows hold
+// a codeword's 16-byte chunks XOR-swizzled by row so that the 32 rows of an A
+// fragment fall on distinct banks for 8- and 16-lane read groups alike.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -35,191 +52,426 @@ namespace fkv {
 namespace {
 
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef _Float16 half2 __attribute__((ext_vector_type(2)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-constexpr int kWaves = 4;
-constexpr int kThreads = 64 * kWaves;
+constexpr int kLdsBudget = 160 * 1024;
+constexpr float kBiasHiScale = 16384.0f;   // weight of the bias's second fp16 slot
+
+constexpr int pow2ceil(int v) { return v <= 1 ? 1 : 2 * pow2ceil((v + 1) / 2); }
 
 template <int D>
-struct Shape {
-    static constexpr int KS = D / 16;              // 16-deep matrix steps along d
-    static constexpr int ROW = D + 8;              // LDS row stride in halfs (16-byte pad)
-    static constexpr int TT = D <= 64 ? 2 : 1;     // 32-token tiles per wave
-    static constexpr int TOK = kWaves * TT * 32;   // tokens per block
+struct Cfg {
+    static constexpr int KS = D / 16;                    // 16-deep matrix steps along d
+    static constexpr int NCH = D / 8;                    // 16-byte chunks of a codeword
+    static constexpr int CPR = pow2ceil(NCH);            // chunks per LDS row (power of two)
+    static constexpr int TT = D <= 64 ? 2 : 1;           // 32-token tiles per wave
+    static constexpr int WAVES = D <= 64 ? 4 : 8;
+    static constexpr int THREADS = 64 * WAVES;
+    static constexpr int TOK = WAVES * TT * 32;          // tokens per block
+    static constexpr int MIN_BLOCKS = 8 / WAVES;         // two waves per SIMD
+    static constexpr int ROW_BYTES = CPR * 16;
+    static constexpr int BUF_ROW = ROW_BYTES + 16;       // book row + its bias-step A row
+    // two book buffers when two full (K = 256) books fit, else one
+    static constexpr int NBUF = 2 * 256 * BUF_ROW <= kLdsBudget ? 2 : 1;
 };
 
-inline size_t rvq_lds_bytes(int D, int Kp)
+// Slot of chunk p in LDS row r.  Makes any 16 consecutive rows (aligned to 16)
+// hit 16 distinct 16-byte bank groups, and any aligned 8 rows 8 distinct ones.
+template <int D>
+__device__ __forceinline__ int swz(int r, int p)
 {
-    return (size_t)Kp * (D + 8) * sizeof(_Float16) + (size_t)Kp * sizeof(float);
+    constexpr int CPR = Cfg<D>::CPR;
+    if (CPR >= 16) return p ^ (r & 15);
+    if (CPR == 8) return p ^ ((r + (r >> 3)) & 7);
+    if (CPR == 4) return p ^ (((r >> 1) + (r >> 3)) & 3);
+    return p ^ (((r >> 2) ^ (r >> 3)) & 1);
 }
 
 template <int D>
-__global__ __launch_bounds__(kThreads) void rvq_assign_kernel(
+size_t lds_bytes(int Kp)
+{
+    return (size_t)Cfg<D>::NBUF * Kp * Cfg<D>::BUF_ROW;
+}
+
+// Asynchronously copies stage codebook C ([K][D] fp16) into an LDS buffer of
+// Kp swizzled rows.  Padding slots and rows >= K are loaded from a valid dummy
+// address; their scores are forced to -inf by the bias step.
+template <int D>
+__device__ __forceinline__ void book_to_lds_async(const _Float16* __restrict__ C, int K, int Kp,
+                                                  uint8_t* buf, int wave, int lane)
+{
+    constexpr int CPR = Cfg<D>::CPR, W = Cfg<D>::WAVES;
+    const int chunks = Kp * CPR;
+    for (int q0 = wave * 64; q0 < chunks; q0 += W * 64) {
+        const int q = q0 + lane;
+        const int r = q / CPR;
+        const int p = swz<D>(r, q % CPR);
+        const _Float16* src = (r < K && p < Cfg<D>::NCH) ? C + (size_t)r * D + p * 8 : C;
+        __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)src,
+                                         (void __attribute__((address_space(3)))*)(buf + (size_t)q0 * 16),
+                                         16, 0, 0);
+    }
+}
+
+// Bias-step A rows of a book buffer: (-||c||^2/2 as hi + mid + lo fp16 parts,
+// 1, 2^14, 0, 0, 0); rows >= K start at -inf.
+template <int D>
+__device__ __forceinline__ void book_bias_rows(uint8_t* buf, int K, int Kp)
+{
+    half8* arow = (half8*)(buf + (size_t)Kp * Cfg<D>::ROW_BYTES);
+    for (int r = threadIdx.x; r < Kp; r += Cfg<D>::THREADS) {
+        float acc = 0.0f;
+#pragma unroll
+        for (int p = 0; p < Cfg<D>::NCH; ++p) {
+            const half8 v = *(const half8*)(buf + ((size_t)r * Cfg<D>::CPR + swz<D>(r, p)) * 16);
+#pragma unroll
+            for (int e = 0; e < 8; e += 2) {
+                const half2 h = {v[e], v[e + 1]};
+                acc = __builtin_amdgcn_fdot2(h, h, acc, false);
+            }
+        }
+        const float n = -0.5f * acc;
+        const _Float16 hi = (_Float16)n;
+        const float rem = n - (float)hi;
+        const _Float16 mid = (_Float16)rem;
+        const _Float16 lo = (_Float16)(rem - (float)mid);
+        half8 a = (half8)(_Float16)0;
+        a[0] = r < K ? hi : (_Float16)(-INFINITY);
+        a[1] = r < K ? mid : (_Float16)0;
+        a[2] = r < K ? lo : (_Float16)0;
+        a[3] = (_Float16)1.0f;
+        a[4] = (_Float16)kBiasHiScale;
+        arow[r] = a;
+    }
+}
+
+// Bias-step B column of a token: slots 0-2 multiply the norm parts (1, 1, 1),
+// slots 3-4 hold -b rounded up in magnitude, b <= 32768 in slot 3 directly,
+// larger b in slot 4 in units of 2^14.  Lanes holding k = 8..15 give zeros.
+__device__ __forceinline__ half8 bias_column(float b, int hh)
+{
+    half8 v = (half8)(_Float16)0;
+    if (hh == 0) {
+        const float bu = fmaxf(b * (1.0f + 0x1p-9f), 0x1p-24f);
+        v[0] = v[1] = v[2] = (_Float16)1.0f;
+        if (bu <= 32768.0f)
+            v[3] = (_Float16)(-bu);
+        else
+            v[4] = (_Float16)(-fminf(bu * (1.0f / kBiasHiScale), 65504.0f));
+    }
+    return v;
+}
+
+__device__ __forceinline__ void wait_all_and_sync()
+{
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+}
+
+// A-operand fragments of one 32-codeword tile: its d/16 data steps and the
+// bias step (zero for the lanes that hold k = 8..15).
+template <int D>
+struct Frag {
+    half8 a[Cfg<D>::KS];
+    half8 bias;
+};
+
+template <int D>
+__device__ __forceinline__ void load_frag(Frag<D>& f, const uint8_t* buf, const half8* abias_rows, int ct,
+                                          int col, int hh)
+{
+    const int arow = ct * 32 + col;
+    const half8 bz = abias_rows[arow];
+    f.bias = hh == 0 ? bz : (half8)(_Float16)0;
+    const uint8_t* abase = buf + (size_t)arow * Cfg<D>::ROW_BYTES;
+#pragma unroll
+    for (int ks = 0; ks < Cfg<D>::KS; ++ks) f.a[ks] = *(const half8*)(abase + swz<D>(arow, 2 * ks + hh) * 16);
+}
+
+// acc[tt] = bias step + A(tile) x B(tt) over all k-steps; with TWO a second B
+// operand accumulates into the same tile.
+template <int D, int TT, bool TWO>
+__device__ __forceinline__ void issue_tile(const Frag<D>& f, const half8 (&bz)[TT],
+                                           const half8 (&bA)[TT][Cfg<D>::KS],
+                                           const half8 (&bB)[TT][Cfg<D>::KS], floatx16 (&acc)[TT])
+{
+#pragma unroll
+    for (int tt = 0; tt < TT; ++tt)
+        acc[tt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(f.bias, bz[tt], (floatx16)0.0f, 0, 0, 0);
+#pragma unroll
+    for (int ks = 0; ks < Cfg<D>::KS; ++ks) {
+#pragma unroll
+        for (int tt = 0; tt < TT; ++tt)
+            acc[tt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(f.a[ks], bA[tt][ks], acc[tt], 0, 0, 0);
+        if (TWO) {
+#pragma unroll
+            for (int tt = 0; tt < TT; ++tt)
+                acc[tt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(f.a[ks], bB[tt][ks], acc[tt], 0, 0, 0);
+        }
+    }
+}
+
+// Minimum over a lane's 16 scores of (float bits with the low 4 bits replaced
+// by the register index), as a tree of three-input minima.
+__device__ __forceinline__ uint32_t tile_min_key(const floatx16& a)
+{
+    uint32_t k[16];
+#pragma unroll
+    for (int v = 0; v < 16; ++v) k[v] = (__float_as_uint(a[v]) & ~15u) | (uint32_t)v;
+    const uint32_t m0 = min(min(k[0], k[1]), k[2]);
+    const uint32_t m1 = min(min(k[3], k[4]), k[5]);
+    const uint32_t m2 = min(min(k[6], k[7]), k[8]);
+    const uint32_t m3 = min(min(k[9], k[10]), k[11]);
+    const uint32_t m4 = min(min(k[12], k[13]), k[14]);
+    const uint32_t m5 = min(min(m0, m1), m2);
+    const uint32_t m6 = min(min(m3, m4), k[15]);
+    return min(m5, m6);
+}
+
+// Folds a finished tile into the running best key of each token tile; the
+// earlier tile wins ties on the value bits.
+template <int TT>
+__device__ __forceinline__ void merge_tile(const floatx16 (&acc)[TT], int ct, uint32_t (&bkey)[TT],
+                                           int (&bct)[TT])
+{
+#pragma unroll
+    for (int tt = 0; tt < TT; ++tt) {
+        const uint32_t k = tile_min_key(acc[tt]);
+        if ((k & ~15u) < (bkey[tt] & ~15u)) {
+            bkey[tt] = k;
+            bct[tt] = ct;
+        }
+    }
+}
+
+// Instruction-interleaving hints for one pipelined step: every MFMA of the tile
+// being issued is followed by a few VALU ops of the previous tile's argmin and,
+// early on, the LDS reads of the next tile's fragments, so one wave keeps its
+// matrix core busy while its vector ALU and LDS work proceed.
+template <int NMFMA, int NVALU, int NDS>
+__device__ __forceinline__ void interleave_hint()
+{
+    constexpr int per = (NVALU + NMFMA - 1) / NMFMA;
+#pragma unroll
+    for (int i = 0; i < NMFMA; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);      // one MFMA
+        if (i < NDS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+        __builtin_amdgcn_sched_group_barrier(0x002, per, 0);    // a few VALU
+    }
+}
+
+// One stage's scores over all nct (even) codeword tiles, software-pipelined:
+// the fragments of tile ct+2 load and the MFMAs of tile ct+1 run while the
+// argmin of tile ct executes on the VALU.
+template <int D, int TT, bool TWO>
+__device__ __forceinline__ void stage_scan(const uint8_t* buf, const half8* abias_rows, int nct, int col,
+                                           int hh, const half8 (&bz)[TT], const half8 (&bA)[TT][Cfg<D>::KS],
+                                           const half8 (&bB)[TT][Cfg<D>::KS], uint32_t (&bkey)[TT],
+                                           int (&bct)[TT])
+{
+    constexpr int NM = TT * (1 + Cfg<D>::KS * (TWO ? 2 : 1));   // MFMAs per tile
+    constexpr int NV = TT * 30;                                 // VALU ops of one tile's argmin
+    constexpr int ND = Cfg<D>::KS + 1;                          // LDS reads of one tile's fragments
+    Frag<D> f0, f1;
+    floatx16 acc0[TT], acc1[TT];
+    load_frag<D>(f0, buf, abias_rows, 0, col, hh);
+    load_frag<D>(f1, buf, abias_rows, 1, col, hh);
+    issue_tile<D, TT, TWO>(f0, bz, bA, bB, acc0);
+    int ct = 0;
+    for (; ct + 2 < nct; ct += 2) {
+        issue_tile<D, TT, TWO>(f1, bz, bA, bB, acc1);
+        load_frag<D>(f0, buf, abias_rows, ct + 2, col, hh);
+        merge_tile<TT>(acc0, ct, bkey, bct);
+        interleave_hint<NM, NV, ND>();
+        issue_tile<D, TT, TWO>(f0, bz, bA, bB, acc0);
+        load_frag<D>(f1, buf, abias_rows, min(ct + 3, nct - 1), col, hh);
+        merge_tile<TT>(acc1, ct + 1, bkey, bct);
+        interleave_hint<NM, NV, ND>();
+    }
+    issue_tile<D, TT, TWO>(f1, bz, bA, bB, acc1);
+    merge_tile<TT>(acc0, ct, bkey, bct);
+    merge_tile<TT>(acc1, ct + 1, bkey, bct);
+}
+
+template <int D, bool HILO>
+__global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assign_kernel(
     const _Float16* __restrict__ x, const _Float16* __restrict__ books,
     const int32_t* __restrict__ stream_book, uint8_t* __restrict__ symbols,
     float* __restrict__ residual, uint32_t* __restrict__ n_bad, int64_t T, int64_t t_begin,
     int64_t Ta, int S, int K, int Kp, int n_books, int64_t blocks_per_stream)
 {
-    constexpr int KS = Shape<D>::KS, ROW = Shape<D>::ROW, TT = Shape<D>::TT, TOK = Shape<D>::TOK;
+    using C = Cfg<D>;
+    constexpr int KS = C::KS, TT = C::TT, TOK = C::TOK, NBUF = C::NBUF;
     extern __shared__ __align__(16) uint8_t lds[];
-    _Float16* sB = (_Float16*)lds;
-    float* sN = (float*)(lds + (size_t)Kp * ROW * sizeof(_Float16));
+    // LDS: NBUF buffers, each Kp swizzled book rows then Kp bias-step A rows;
+    // addressed from `lds` so every access stays an LDS access.
+    const size_t buf_bytes = (size_t)Kp * C::BUF_ROW;
 
-    const int64_t s = blockIdx.x / blocks_per_stream;
-    const int64_t tb = (blockIdx.x - s * blocks_per_stream) * TOK;
+    // XCD-aware order: blocks dispatched to one XCD (every 8th) take consecutive
+    // work items, so the blocks of one stream share that XCD's L2 copy of its book.
+    const uint32_t nblk = gridDim.x, q8 = nblk / 8, r8 = nblk % 8;
+    const uint32_t xcd = blockIdx.x % 8, slot = blockIdx.x / 8;
+    const int64_t item = (int64_t)xcd * q8 + min(xcd, r8) + slot;
+    const int64_t s = item / blocks_per_stream;
+    const int64_t tb = (item - s * blocks_per_stream) * TOK;
+
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int col = lane & 31, hh = lane >> 5;
     uint8_t* sym_s = symbols + s * Ta * S;
     const int b = stream_book[s];
     if (b < 0 || b >= n_books) {
         const int64_t te = min(Ta, tb + TOK);
-        for (int64_t i = tb * S + tid; i < te * S; i += kThreads) sym_s[i] = 0xFF;
+        for (int64_t i = tb * S + tid; i < te * S; i += C::THREADS) sym_s[i] = 0xFF;
         if (residual)
-            for (int64_t i = tb * D + tid; i < te * D; i += kThreads) residual[s * Ta * D + i] = NAN;
+            for (int64_t i = tb * D + tid; i < te * D; i += C::THREADS) residual[s * Ta * D + i] = NAN;
         if (tid == 0 && tb == 0 && n_bad) atomicAdd(n_bad, 1u);
         return;
     }
     const _Float16* bk = books + (int64_t)b * S * K * D;
 
+    // prologue: start the first books' copies, then load this lane's tokens
+    book_to_lds_async<D>(bk, K, Kp, lds, wave, lane);
+    if (NBUF > 1 && S > 1) book_to_lds_async<D>(bk + (size_t)K * D, K, Kp, lds + buf_bytes, wave, lane);
+
     int64_t tok[TT];
     bool valid[TT];
-    float r32[TT][KS][8];
-    half8 bh[TT][KS], bl[TT][KS];
+    half8 bA[TT][KS], bB[TT][KS];   // B operands of the current stage's passes
+    half8 bz[TT];                   // bias-step B operand
 #pragma unroll
     for (int tt = 0; tt < TT; ++tt) {
         tok[tt] = tb + (int64_t)(wave * TT + tt) * 32 + col;
         valid[tt] = tok[tt] < Ta;
         const _Float16* row = x + (s * T + t_begin + (valid[tt] ? tok[tt] : 0)) * D + 8 * hh;
+        float n2 = 0.0f;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-            half8 v = valid[tt] ? *(const half8*)(row + 16 * ks) : (half8)(_Float16)0;
-            bh[tt][ks] = -v;
-            bl[tt][ks] = (half8)(_Float16)0;
+            const half8 v = valid[tt] ? *(const half8*)(row + 16 * ks) : (half8)(_Float16)0;
+            bA[tt][ks] = v;
+            bB[tt][ks] = (half8)(_Float16)0;
 #pragma unroll
-            for (int e = 0; e < 8; ++e) r32[tt][ks][e] = (float)v[e];
+            for (int e = 0; e < 8; e += 2) {
+                const half2 h = {v[e], v[e + 1]};
+                n2 = __builtin_amdgcn_fdot2(h, h, n2, false);
+            }
         }
+        n2 += __shfl_xor(n2, 32);
+        bz[tt] = bias_column(0.5f * n2 * (1.0f + 0x1p-10f), hh);
     }
 
-    for (int st = 0; st < S; ++st) {
-        // Stage this stage's codebook (rows >= K zero) and its half norms.
-        __syncthreads();
-        const _Float16* C = bk + (int64_t)st * K * D;
-        for (int i = tid; i < Kp * (D / 8); i += kThreads) {
-            const int rw = i / (D / 8), c8 = i - rw * (D / 8);
-            half8 v = rw < K ? *(const half8*)(C + (int64_t)rw * D + c8 * 8) : (half8)(_Float16)0;
-            *(half8*)(sB + rw * ROW + c8 * 8) = v;
-        }
-        __syncthreads();
-        for (int i = tid; i < Kp; i += kThreads) {
-            float acc = 0.0f;
-            for (int c8 = 0; c8 < D / 8; ++c8) {
-                const half8 v = *(const half8*)(sB + i * ROW + c8 * 8);
-#pragma unroll
-                for (int e = 0; e < 8; ++e) acc += (float)v[e] * (float)v[e];
-            }
-            sN[i] = i < K ? 0.5f * acc : INFINITY;
-        }
-        __syncthreads();
+    wait_all_and_sync();
+    book_bias_rows<D>(lds, K, Kp);
+    if (NBUF > 1 && S > 1) book_bias_rows<D>(lds + buf_bytes, K, Kp);
+    __syncthreads();
 
-        float best[TT];
-        int bidx[TT];
+    const int nct = Kp / 32;  // even
+    for (int st = 0; st < S; ++st) {
+        const int cur = NBUF > 1 ? (st & 1) : 0;
+        const uint8_t* buf = lds + cur * buf_bytes;
+        const half8* abias_rows = (const half8*)(buf + (size_t)Kp * C::ROW_BYTES);
+        const bool two = st > 0;
+        uint32_t bkey[TT];
+        int bct[TT];
 #pragma unroll
         for (int tt = 0; tt < TT; ++tt) {
-            best[tt] = INFINITY;
-            bidx[tt] = 0;
+            bkey[tt] = 0xFFFFFFFFu;
+            bct[tt] = 0;
         }
-        for (int ct = 0; ct < Kp / 32; ++ct) {
-            const float* nb = sN + ct * 32 + 4 * hh;
-            const floatx4 n0 = *(const floatx4*)(nb + 0), n1 = *(const floatx4*)(nb + 8);
-            const floatx4 n2 = *(const floatx4*)(nb + 16), n3 = *(const floatx4*)(nb + 24);
-            floatx16 acc[TT];
-#pragma unroll
-            for (int tt = 0; tt < TT; ++tt) {
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    acc[tt][e] = n0[e];
-                    acc[tt][4 + e] = n1[e];
-                    acc[tt][8 + e] = n2[e];
-                    acc[tt][12 + e] = n3[e];
-                }
-            }
-            const _Float16* arow = sB + (ct * 32 + col) * ROW + 8 * hh;
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                const half8 a = *(const half8*)(arow + 16 * ks);
-#pragma unroll
-                for (int tt = 0; tt < TT; ++tt)
-                    acc[tt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, bh[tt][ks], acc[tt], 0, 0, 0);
-                if (st > 0) {
-#pragma unroll
-                    for (int tt = 0; tt < TT; ++tt)
-                        acc[tt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, bl[tt][ks], acc[tt], 0, 0, 0);
-                }
-            }
-            // acc[tt][v] is the score of codeword ct*32 + 8(v/4) + 4*hh + v%4 for
-            // token col: increasing v visits this lane's codewords in index order.
-#pragma unroll
-            for (int tt = 0; tt < TT; ++tt) {
-#pragma unroll
-                for (int v = 0; v < 16; ++v) {
-                    const float val = acc[tt][v];
-                    if (val < best[tt]) {
-                        best[tt] = val;
-                        bidx[tt] = ct * 32 + 8 * (v >> 2) + 4 * hh + (v & 3);
-                    }
-                }
-            }
-        }
+        if (two)
+            stage_scan<D, TT, true>(buf, abias_rows, nct, col, hh, bz, bA, bB, bkey, bct);
+        else
+            stage_scan<D, TT, false>(buf, abias_rows, nct, col, hh, bz, bA, bB, bkey, bct);
 #pragma unroll
         for (int tt = 0; tt < TT; ++tt) {
-            const float ob = __shfl_xor(best[tt], 32);
-            const int oi = __shfl_xor(bidx[tt], 32);
-            if (ob < best[tt] || (ob == best[tt] && oi < bidx[tt])) {
-                best[tt] = ob;
-                bidx[tt] = oi;
+            const int li = (int)(bkey[tt] & 15u);
+            int cw = bct[tt] * 32 + 8 * (li >> 2) + 4 * hh + (li & 3);
+            cw = min(cw, K - 1);  // only reachable with all-NaN scores; keeps reads in bounds
+            uint32_t val = bkey[tt] & ~15u;
+            const uint32_t oval = __shfl_xor(val, 32);
+            const int ocw = __shfl_xor(cw, 32);
+            if (oval < val || (oval == val && ocw < cw)) {
+                val = oval;
+                cw = ocw;
             }
-            if (hh == 0 && valid[tt]) sym_s[tok[tt] * S + st] = (uint8_t)bidx[tt];
-            const _Float16* crow = sB + bidx[tt] * ROW + 8 * hh;
+            if (hh == 0 && valid[tt]) sym_s[tok[tt] * S + st] = (uint8_t)cw;
+            // next stage's bias: this stage's winning |u| grown by 2^-10
+            bz[tt] = bias_column(-__uint_as_float(val) * (1.0f + 0x1p-10f), hh);
+            // this lane's chunks of the chosen codeword
+            half8 cv[KS];
+            const uint8_t* crow = buf + (size_t)cw * C::ROW_BYTES;
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                const half8 cv = *(const half8*)(crow + 16 * ks);
-#pragma unroll
-                for (int e = 0; e < 8; ++e) r32[tt][ks][e] -= (float)cv[e];
-            }
-            if (st + 1 < S) {
+            for (int ks = 0; ks < KS; ++ks) cv[ks] = *(const half8*)(crow + swz<D>(cw, 2 * ks + hh) * 16);
+            const bool last = st + 1 == S;
+            if (HILO && st >= 1 && !last) {
+                // r = (hi + lo) - c for st >= 2, (x - c_0) - c_1 for st == 1; split again
 #pragma unroll
                 for (int ks = 0; ks < KS; ++ks) {
 #pragma unroll
                     for (int e = 0; e < 8; ++e) {
-                        const _Float16 h = (_Float16)r32[tt][ks][e];
-                        const _Float16 l = (_Float16)(r32[tt][ks][e] - (float)h);
-                        bh[tt][ks][e] = -h;
-                        bl[tt][ks][e] = -l;
+                        const float rv = (float)bA[tt][ks][e] + (float)bB[tt][ks][e] - (float)cv[ks][e];
+                        const _Float16 h = (_Float16)rv;
+                        bA[tt][ks][e] = h;
+                        bB[tt][ks][e] = (_Float16)(rv - (float)h);
                     }
                 }
             }
-        }
-    }
-
-    if (residual) {
+            if (last && residual && valid[tt]) {
+                float* out = residual + (s * Ta + tok[tt]) * D + 8 * hh;
 #pragma unroll
-        for (int tt = 0; tt < TT; ++tt) {
-            if (!valid[tt]) continue;
-            float* out = residual + (s * Ta + tok[tt]) * D + 8 * hh;
+                for (int ks = 0; ks < KS; ++ks) {
+                    floatx4 lo4, hi4;
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                floatx4 lo4, hi4;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    lo4[e] = r32[tt][ks][e];
-                    hi4[e] = r32[tt][ks][4 + e];
+                    for (int e = 0; e < 8; ++e) {
+                        const float rv = (float)bA[tt][ks][e] + (st > 0 ? (float)bB[tt][ks][e] : 0.0f) -
+                                         (float)cv[ks][e];
+                        if (e < 4) lo4[e] = rv; else hi4[e - 4] = rv;
+                    }
+                    *(floatx4*)(out + 16 * ks) = lo4;
+                    *(floatx4*)(out + 16 * ks + 4) = hi4;
                 }
-                *(floatx4*)(out + 16 * ks) = lo4;
-                *(floatx4*)(out + 16 * ks + 4) = hi4;
+            }
+            if (st == 0 && !last) {
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) bB[tt][ks] = -cv[ks];
             }
         }
+        if (st + 1 < S) {
+            // Book pipeline: buffer `cur` is free once every wave is past here.
+            wait_all_and_sync();
+            if (NBUF == 1) {
+                book_to_lds_async<D>(bk + (size_t)(st + 1) * K * D, K, Kp, lds, wave, lane);
+                wait_all_and_sync();
+            } else if (st + 2 < S) {
+                book_to_lds_async<D>(bk + (size_t)(st + 2) * K * D, K, Kp, lds + cur * buf_bytes, wave, lane);
+            }
+            if (NBUF == 1 || st >= 1) book_bias_rows<D>(lds + (NBUF > 1 ? ((st + 1) & 1) : 0) * buf_bytes, K, Kp);
+            __syncthreads();
+        }
     }
+}
+
+template <int D, bool HILO>
+int launch_rvq_t(const fkv_rvq_desc* dsc, const uint16_t* x, const uint16_t* books,
+                 const int32_t* stream_book, uint8_t* symbols, float* residual, uint32_t* n_bad,
+                 hipStream_t stream)
+{
+    static std::once_flag once;
+    const int Kp = (dsc->K + 63) / 64 * 64;  // whole pairs of 32-codeword tiles
+    std::call_once(once, [] {
+        (void)hipFuncSetAttribute((const void*)rvq_assign_kernel<D, HILO>,
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes<D>(256));
+    });
+    (void)hipGetLastError();
+    const int64_t Ta = dsc->t_end - dsc->t_begin;
+    const int64_t bps = (Ta + Cfg<D>::TOK - 1) / Cfg<D>::TOK;
+    const int64_t nblk = bps * dsc->n_streams;
+    if (nblk > 0x7fffffff) return FKV_ERR_UNSUPPORTED;
+    hipLaunchKernelGGL((rvq_assign_kernel<D, HILO>), dim3((unsigned)nblk), dim3(Cfg<D>::THREADS),
+                       lds_bytes<D>(Kp), stream, (const _Float16*)x, (const _Float16*)books, stream_book,
+                       symbols, residual, n_bad, dsc->T, dsc->t_begin, Ta, dsc->S, dsc->K, Kp,
+                       dsc->n_books, bps);
+    return launch_status();
 }
 
 template <int D>
@@ -227,22 +479,9 @@ int launch_rvq(const fkv_rvq_desc* dsc, const uint16_t* x, const uint16_t* books
                const int32_t* stream_book, uint8_t* symbols, float* residual, uint32_t* n_bad,
                hipStream_t stream)
 {
-    static std::once_flag once;
-    const int Kp = (dsc->K + 31) / 32 * 32;
-    const size_t shm = rvq_lds_bytes(D, Kp);
-    std::call_once(once, [] {
-        (void)hipFuncSetAttribute((const void*)rvq_assign_kernel<D>,
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)rvq_lds_bytes(D, 256));
-    });
-    (void)hipGetLastError();
-    const int64_t Ta = dsc->t_end - dsc->t_begin;
-    const int64_t bps = (Ta + Shape<D>::TOK - 1) / Shape<D>::TOK;
-    const int64_t nblk = bps * dsc->n_streams;
-    if (nblk > 0x7fffffff) return FKV_ERR_UNSUPPORTED;
-    hipLaunchKernelGGL(rvq_assign_kernel<D>, dim3((unsigned)nblk), dim3(kThreads), shm, stream,
-                       (const _Float16*)x, (const _Float16*)books, stream_book, symbols, residual,
-                       n_bad, dsc->T, dsc->t_begin, Ta, dsc->S, dsc->K, Kp, dsc->n_books, bps);
-    return launch_status();
+    if (dsc->S <= 2)
+        return launch_rvq_t<D, false>(dsc, x, books, stream_book, symbols, residual, n_bad, stream);
+    return launch_rvq_t<D, true>(dsc, x, books, stream_book, symbols, residual, n_bad, stream);
 }
 
 }  // namespace
