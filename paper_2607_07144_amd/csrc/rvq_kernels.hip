@@ -20,13 +20,14 @@
 //   * the d/16 data steps add r.c_i.
 // In the 32x32 accumulator layout lane l owns token l%32 and 16 of the tile's
 // 32 codewords, so the argmin is in-lane: a negative float's bits, read as an
-// unsigned integer, grow with its magnitude; with the low 4 bits replaced by
-// the codeword's position among the lane's 16 they form a key whose minimum
-// (v_min3_u32) is the nearest codeword and carries its index.  Dropping 4
-// mantissa bits coarsens the comparison to 2^-19 relative, well inside the
-// 1e-5 near-tie band.  Tiles merge on the value bits (earlier tile wins ties),
-// then lane l with lane l^32.  Stage s's bias is the winning |u| of stage s-1
-// (||r_s||^2/2 plus the previous margin), grown by 2^-10.
+// unsigned integer, grow with its magnitude; with the low 5 bits replaced by
+// the codeword's position among the 32 that the lane holds in a pair of
+// consecutive tiles, they form a key whose minimum (v_min3_u32) is the
+// nearest codeword and carries its index.  Dropping 5 mantissa bits coarsens
+// the comparison to 2^-18 relative, inside the 1e-5 near-tie band.  Tile pairs
+// merge on the value bits (earlier pair wins ties), then lane l with lane
+// l^32.  Stage s's bias is the winning |u| of stage s-1 (||r_s||^2/2 plus the
+// previous margin), grown by 2^-10.
 //
 // Exact operands.  Stage 0 multiplies fp16 x by fp16 codewords (every product
 // exact in fp32).  Stage 1 uses r_1 = x - c_0 as two fp16 passes, x.c and
@@ -73,26 +74,36 @@ struct Cfg {
     static constexpr int MIN_BLOCKS = 8 / WAVES;         // two waves per SIMD
     static constexpr int ROW_BYTES = CPR * 16;
     static constexpr int BUF_ROW = ROW_BYTES + 16;       // book row + its bias-step A row
+    static constexpr int TILE_BYTES = 32 * ROW_BYTES;    // one 32-codeword tile of a book
     // two book buffers when two full (K = 256) books fit, else one
-    static constexpr int NBUF = 2 * 256 * BUF_ROW <= kLdsBudget ? 2 : 1;
+    static constexpr int NBUF = 2 * (256 * BUF_ROW + 16) <= kLdsBudget ? 2 : 1;
 };
 
-// Slot of chunk p in LDS row r.  Makes any 16 consecutive rows (aligned to 16)
-// hit 16 distinct 16-byte bank groups, and any aligned 8 rows 8 distinct ones.
+// Slot of chunk p in LDS row r.  Depends only on the row's place in its
+// 32-row tile (so a lane's fragment offsets are the same in every tile) and
+// makes any aligned 16 rows hit 16 distinct 16-byte bank groups, any aligned
+// 8 rows 8 distinct ones.
 template <int D>
 __device__ __forceinline__ int swz(int r, int p)
 {
     constexpr int CPR = Cfg<D>::CPR;
+    r &= 31;
     if (CPR >= 16) return p ^ (r & 15);
     if (CPR == 8) return p ^ ((r + (r >> 3)) & 7);
     if (CPR == 4) return p ^ (((r >> 1) + (r >> 3)) & 3);
     return p ^ (((r >> 2) ^ (r >> 3)) & 1);
 }
 
+// One LDS book buffer: Kp swizzled rows, Kp bias-step A rows, one zero chunk.
+__host__ __device__ constexpr size_t buf_bytes_of(int row_bytes, int Kp)
+{
+    return (size_t)Kp * (row_bytes + 16) + 16;
+}
+
 template <int D>
 size_t lds_bytes(int Kp)
 {
-    return (size_t)Cfg<D>::NBUF * Kp * Cfg<D>::BUF_ROW;
+    return (size_t)Cfg<D>::NBUF * buf_bytes_of(Cfg<D>::ROW_BYTES, Kp);
 }
 
 // Asynchronously copies stage codebook C ([K][D] fp16) into an LDS buffer of
@@ -171,23 +182,42 @@ __device__ __forceinline__ void wait_all_and_sync()
 }
 
 // A-operand fragments of one 32-codeword tile: its d/16 data steps and the
-// bias step (zero for the lanes that hold k = 8..15).
+// bias step (a zero chunk for the lanes that hold k = 8..15).
 template <int D>
 struct Frag {
     half8 a[Cfg<D>::KS];
     half8 bias;
 };
 
+// Per-lane LDS byte offsets of a lane's fragments inside tile 0 of a buffer;
+// tile ct adds ct * TILE_BYTES to the data and ct * bias_step to the bias.
 template <int D>
-__device__ __forceinline__ void load_frag(Frag<D>& f, const uint8_t* buf, const half8* abias_rows, int ct,
-                                          int col, int hh)
+struct FragAddr {
+    uint32_t a[Cfg<D>::KS];
+    uint32_t bias;
+    uint32_t bias_step;
+};
+
+template <int D>
+__device__ __forceinline__ FragAddr<D> frag_addr(int Kp, int col, int hh)
 {
-    const int arow = ct * 32 + col;
-    const half8 bz = abias_rows[arow];
-    f.bias = hh == 0 ? bz : (half8)(_Float16)0;
-    const uint8_t* abase = buf + (size_t)arow * Cfg<D>::ROW_BYTES;
+    FragAddr<D> fa;
 #pragma unroll
-    for (int ks = 0; ks < Cfg<D>::KS; ++ks) f.a[ks] = *(const half8*)(abase + swz<D>(arow, 2 * ks + hh) * 16);
+    for (int ks = 0; ks < Cfg<D>::KS; ++ks)
+        fa.a[ks] = (uint32_t)(col * Cfg<D>::ROW_BYTES + swz<D>(col, 2 * ks + hh) * 16);
+    const uint32_t bias_rows = (uint32_t)(Kp * Cfg<D>::ROW_BYTES);
+    fa.bias = hh == 0 ? bias_rows + (uint32_t)col * 16 : (uint32_t)(Kp * Cfg<D>::BUF_ROW);
+    fa.bias_step = hh == 0 ? 32 * 16 : 0;
+    return fa;
+}
+
+template <int D>
+__device__ __forceinline__ void load_frag(Frag<D>& f, const uint8_t* buf, const FragAddr<D>& fa, int ct)
+{
+    const uint8_t* tile = buf + (size_t)ct * Cfg<D>::TILE_BYTES;
+#pragma unroll
+    for (int ks = 0; ks < Cfg<D>::KS; ++ks) f.a[ks] = *(const half8*)(tile + fa.a[ks]);
+    f.bias = *(const half8*)(buf + fa.bias + (uint32_t)ct * fa.bias_step);
 }
 
 // acc[tt] = bias step + A(tile) x B(tt) over all k-steps; with TWO a second B
@@ -213,13 +243,14 @@ __device__ __forceinline__ void issue_tile(const Frag<D>& f, const half8 (&bz)[T
     }
 }
 
-// Minimum over a lane's 16 scores of (float bits with the low 4 bits replaced
-// by the register index), as a tree of three-input minima.
+// Minimum over a lane's 16 scores of (float bits with the low 5 bits replaced
+// by base + register index), as a tree of three-input minima.
+template <uint32_t BASE>
 __device__ __forceinline__ uint32_t tile_min_key(const floatx16& a)
 {
     uint32_t k[16];
 #pragma unroll
-    for (int v = 0; v < 16; ++v) k[v] = (__float_as_uint(a[v]) & ~15u) | (uint32_t)v;
+    for (int v = 0; v < 16; ++v) k[v] = (__float_as_uint(a[v]) & ~31u) | (BASE + (uint32_t)v);
     const uint32_t m0 = min(min(k[0], k[1]), k[2]);
     const uint32_t m1 = min(min(k[3], k[4]), k[5]);
     const uint32_t m2 = min(min(k[6], k[7]), k[8]);
@@ -230,18 +261,26 @@ __device__ __forceinline__ uint32_t tile_min_key(const floatx16& a)
     return min(m5, m6);
 }
 
-// Folds a finished tile into the running best key of each token tile; the
-// earlier tile wins ties on the value bits.
+// Key minimum of the first tile of a pair (positions 0..15).
 template <int TT>
-__device__ __forceinline__ void merge_tile(const floatx16 (&acc)[TT], int ct, uint32_t (&bkey)[TT],
-                                           int (&bct)[TT])
+__device__ __forceinline__ void pair_first(const floatx16 (&acc)[TT], uint32_t (&pk)[TT])
+{
+#pragma unroll
+    for (int tt = 0; tt < TT; ++tt) pk[tt] = tile_min_key<0>(acc[tt]);
+}
+
+// Adds the second tile of pair `pair` (positions 16..31) and folds the pair
+// into the running best; an earlier pair wins ties on the value bits.
+template <int TT>
+__device__ __forceinline__ void pair_second(const floatx16 (&acc)[TT], const uint32_t (&pk)[TT], int pair,
+                                            uint32_t (&bkey)[TT], int (&bpair)[TT])
 {
 #pragma unroll
     for (int tt = 0; tt < TT; ++tt) {
-        const uint32_t k = tile_min_key(acc[tt]);
-        if ((k & ~15u) < (bkey[tt] & ~15u)) {
+        const uint32_t k = min(pk[tt], tile_min_key<16>(acc[tt]));
+        if ((k & ~31u) < (bkey[tt] & ~31u)) {
             bkey[tt] = k;
-            bct[tt] = ct;
+            bpair[tt] = pair;
         }
     }
 }
@@ -264,35 +303,36 @@ __device__ __forceinline__ void interleave_hint()
 
 // One stage's scores over all nct (even) codeword tiles, software-pipelined:
 // the fragments of tile ct+2 load and the MFMAs of tile ct+1 run while the
-// argmin of tile ct executes on the VALU.
+// argmin of tile ct executes on the VALU.  Tiles 2p and 2p+1 form pair p.
 template <int D, int TT, bool TWO>
-__device__ __forceinline__ void stage_scan(const uint8_t* buf, const half8* abias_rows, int nct, int col,
-                                           int hh, const half8 (&bz)[TT], const half8 (&bA)[TT][Cfg<D>::KS],
+__device__ __forceinline__ void stage_scan(const uint8_t* buf, const FragAddr<D>& fa, int nct,
+                                           const half8 (&bz)[TT], const half8 (&bA)[TT][Cfg<D>::KS],
                                            const half8 (&bB)[TT][Cfg<D>::KS], uint32_t (&bkey)[TT],
-                                           int (&bct)[TT])
+                                           int (&bpair)[TT])
 {
     constexpr int NM = TT * (1 + Cfg<D>::KS * (TWO ? 2 : 1));   // MFMAs per tile
-    constexpr int NV = TT * 30;                                 // VALU ops of one tile's argmin
+    constexpr int NV = TT * 26;                                 // VALU ops of one tile's argmin
     constexpr int ND = Cfg<D>::KS + 1;                          // LDS reads of one tile's fragments
     Frag<D> f0, f1;
     floatx16 acc0[TT], acc1[TT];
-    load_frag<D>(f0, buf, abias_rows, 0, col, hh);
-    load_frag<D>(f1, buf, abias_rows, 1, col, hh);
+    uint32_t pk[TT];
+    load_frag<D>(f0, buf, fa, 0);
+    load_frag<D>(f1, buf, fa, 1);
     issue_tile<D, TT, TWO>(f0, bz, bA, bB, acc0);
     int ct = 0;
     for (; ct + 2 < nct; ct += 2) {
         issue_tile<D, TT, TWO>(f1, bz, bA, bB, acc1);
-        load_frag<D>(f0, buf, abias_rows, ct + 2, col, hh);
-        merge_tile<TT>(acc0, ct, bkey, bct);
+        load_frag<D>(f0, buf, fa, ct + 2);
+        pair_first<TT>(acc0, pk);
         interleave_hint<NM, NV, ND>();
         issue_tile<D, TT, TWO>(f0, bz, bA, bB, acc0);
-        load_frag<D>(f1, buf, abias_rows, min(ct + 3, nct - 1), col, hh);
-        merge_tile<TT>(acc1, ct + 1, bkey, bct);
+        load_frag<D>(f1, buf, fa, min(ct + 3, nct - 1));
+        pair_second<TT>(acc1, pk, ct >> 1, bkey, bpair);
         interleave_hint<NM, NV, ND>();
     }
     issue_tile<D, TT, TWO>(f1, bz, bA, bB, acc1);
-    merge_tile<TT>(acc0, ct, bkey, bct);
-    merge_tile<TT>(acc1, ct + 1, bkey, bct);
+    pair_first<TT>(acc0, pk);
+    pair_second<TT>(acc1, pk, ct >> 1, bkey, bpair);
 }
 
 template <int D, bool HILO>
@@ -305,9 +345,9 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
     using C = Cfg<D>;
     constexpr int KS = C::KS, TT = C::TT, TOK = C::TOK, NBUF = C::NBUF;
     extern __shared__ __align__(16) uint8_t lds[];
-    // LDS: NBUF buffers, each Kp swizzled book rows then Kp bias-step A rows;
-    // addressed from `lds` so every access stays an LDS access.
-    const size_t buf_bytes = (size_t)Kp * C::BUF_ROW;
+    // LDS: NBUF buffers, each Kp swizzled book rows, Kp bias-step A rows and a
+    // zero chunk; addressed from `lds` so every access stays an LDS access.
+    const size_t buf_bytes = buf_bytes_of(C::ROW_BYTES, Kp);
 
     // XCD-aware order: blocks dispatched to one XCD (every 8th) take consecutive
     // work items, so the blocks of one stream share that XCD's L2 copy of its book.
@@ -321,6 +361,24 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
     const int col = lane & 31, hh = lane >> 5;
     uint8_t* sym_s = symbols + s * Ta * S;
     const int b = stream_book[s];
+
+    // this lane's tokens (independent of the book id, so their loads overlap its)
+    int64_t tok[TT];
+    bool valid[TT];
+    half8 bA[TT][KS], bB[TT][KS];   // B operands of the current stage's passes
+    half8 bz[TT];                   // bias-step B operand
+#pragma unroll
+    for (int tt = 0; tt < TT; ++tt) {
+        tok[tt] = tb + (int64_t)(wave * TT + tt) * 32 + col;
+        valid[tt] = tok[tt] < Ta;
+        const _Float16* row = x + (s * T + t_begin + (valid[tt] ? tok[tt] : 0)) * D + 8 * hh;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            bA[tt][ks] = valid[tt] ? *(const half8*)(row + 16 * ks) : (half8)(_Float16)0;
+            bB[tt][ks] = (half8)(_Float16)0;
+        }
+    }
+
     if (b < 0 || b >= n_books) {
         const int64_t te = min(Ta, tb + TOK);
         for (int64_t i = tb * S + tid; i < te * S; i += C::THREADS) sym_s[i] = 0xFF;
@@ -331,34 +389,26 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
     }
     const _Float16* bk = books + (int64_t)b * S * K * D;
 
-    // prologue: start the first books' copies, then load this lane's tokens
+    // start the first books' copies; zero chunks for the upper half-wave's bias step
     book_to_lds_async<D>(bk, K, Kp, lds, wave, lane);
     if (NBUF > 1 && S > 1) book_to_lds_async<D>(bk + (size_t)K * D, K, Kp, lds + buf_bytes, wave, lane);
+    if (tid < NBUF) *(half8*)(lds + tid * buf_bytes + (size_t)Kp * C::BUF_ROW) = (half8)(_Float16)0;
 
-    int64_t tok[TT];
-    bool valid[TT];
-    half8 bA[TT][KS], bB[TT][KS];   // B operands of the current stage's passes
-    half8 bz[TT];                   // bias-step B operand
 #pragma unroll
     for (int tt = 0; tt < TT; ++tt) {
-        tok[tt] = tb + (int64_t)(wave * TT + tt) * 32 + col;
-        valid[tt] = tok[tt] < Ta;
-        const _Float16* row = x + (s * T + t_begin + (valid[tt] ? tok[tt] : 0)) * D + 8 * hh;
         float n2 = 0.0f;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-            const half8 v = valid[tt] ? *(const half8*)(row + 16 * ks) : (half8)(_Float16)0;
-            bA[tt][ks] = v;
-            bB[tt][ks] = (half8)(_Float16)0;
 #pragma unroll
             for (int e = 0; e < 8; e += 2) {
-                const half2 h = {v[e], v[e + 1]};
+                const half2 h = {bA[tt][ks][e], bA[tt][ks][e + 1]};
                 n2 = __builtin_amdgcn_fdot2(h, h, n2, false);
             }
         }
         n2 += __shfl_xor(n2, 32);
         bz[tt] = bias_column(0.5f * n2 * (1.0f + 0x1p-10f), hh);
     }
+    const FragAddr<D> fa = frag_addr<D>(Kp, col, hh);
 
     wait_all_and_sync();
     book_bias_rows<D>(lds, K, Kp);
@@ -369,25 +419,24 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
     for (int st = 0; st < S; ++st) {
         const int cur = NBUF > 1 ? (st & 1) : 0;
         const uint8_t* buf = lds + cur * buf_bytes;
-        const half8* abias_rows = (const half8*)(buf + (size_t)Kp * C::ROW_BYTES);
         const bool two = st > 0;
         uint32_t bkey[TT];
-        int bct[TT];
+        int bpair[TT];
 #pragma unroll
         for (int tt = 0; tt < TT; ++tt) {
             bkey[tt] = 0xFFFFFFFFu;
-            bct[tt] = 0;
+            bpair[tt] = 0;
         }
         if (two)
-            stage_scan<D, TT, true>(buf, abias_rows, nct, col, hh, bz, bA, bB, bkey, bct);
+            stage_scan<D, TT, true>(buf, fa, nct, bz, bA, bB, bkey, bpair);
         else
-            stage_scan<D, TT, false>(buf, abias_rows, nct, col, hh, bz, bA, bB, bkey, bct);
+            stage_scan<D, TT, false>(buf, fa, nct, bz, bA, bB, bkey, bpair);
 #pragma unroll
         for (int tt = 0; tt < TT; ++tt) {
-            const int li = (int)(bkey[tt] & 15u);
-            int cw = bct[tt] * 32 + 8 * (li >> 2) + 4 * hh + (li & 3);
+            const int li = (int)(bkey[tt] & 31u);
+            int cw = (2 * bpair[tt] + (li >> 4)) * 32 + 8 * ((li & 15) >> 2) + 4 * hh + (li & 3);
             cw = min(cw, K - 1);  // only reachable with all-NaN scores; keeps reads in bounds
-            uint32_t val = bkey[tt] & ~15u;
+            uint32_t val = bkey[tt] & ~31u;
             const uint32_t oval = __shfl_xor(val, 32);
             const int ocw = __shfl_xor(cw, 32);
             if (oval < val || (oval == val && ocw < cw)) {
@@ -436,7 +485,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
                 for (int ks = 0; ks < KS; ++ks) bB[tt][ks] = -cv[ks];
             }
         }
-        if (st + 1 < S) {
+        if (st + 1 < S && (NBUF == 1 || st >= 1 || st + 2 < S)) {
             // Book pipeline: buffer `cur` is free once every wave is past here.
             wait_all_and_sync();
             if (NBUF == 1) {
