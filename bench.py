@@ -179,6 +179,10 @@ def main():
     ap.add_argument("--cpu-streams", type=int, default=288,
                     help="streams per group the CPU oracle baseline runs on")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="also run one streaming elementwise kernel (torch.neg) that reads and writes "
+                         "this many MiB before the step: a kernel of known traffic for scaling HBM "
+                         "byte counters")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures the path on one GPU; multi-GPU runs are not part of this build "
@@ -189,6 +193,12 @@ def main():
     from paper_2607_07144_amd import fkv
 
     torch.cuda.set_device(0)
+    if args.copy_probe_mib > 0:
+        src = torch.ones(args.copy_probe_mib << 18, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
     cfg, groups = build_workload(args.workload, args.lookups)
     names = ["rvq_assign", "cgr_encode", "cgr_decode", "span_lookup"]
     side = torch.cuda.Stream()
