@@ -37,9 +37,9 @@
 //
 // Codebooks.  Each stage's codebook is copied global -> LDS with the
 // asynchronous global_load_lds_dwordx4 into two alternating buffers, so the
-// next stage's book streams in while the current one is in use.  LDS rows hold
-// a codeword's 16-byte chunks XOR-swizzled by row so that the 32 rows of an A
-// fragment fall on distinct banks for 8- and 16-lane read groups alike.
+// next stage's book streams in while the current one is in use.  An LDS row
+// holds a codeword's 16-byte chunks followed by its bias-step chunk; the odd
+// chunk count per row spreads the 32 rows of an A fragment over distinct banks.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -60,83 +60,71 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 constexpr int kLdsBudget = 160 * 1024;
 constexpr float kBiasHiScale = 16384.0f;   // weight of the bias's second fp16 slot
 
-constexpr int pow2ceil(int v) { return v <= 1 ? 1 : 2 * pow2ceil((v + 1) / 2); }
+// One LDS book buffer: Kp rows of row_p bytes, then a 16-byte zero pad.
+__host__ __device__ constexpr size_t buf_bytes_of(int row_p, int Kp)
+{
+    return (size_t)Kp * row_p + 16;
+}
 
 template <int D>
 struct Cfg {
     static constexpr int KS = D / 16;                    // 16-deep matrix steps along d
     static constexpr int NCH = D / 8;                    // 16-byte chunks of a codeword
-    static constexpr int CPR = pow2ceil(NCH);            // chunks per LDS row (power of two)
+    // LDS row: the codeword's NCH chunks, then its bias-step A chunk.  The odd
+    // number of 16-byte chunks per row puts any 16 consecutive rows on 16
+    // distinct bank groups, so fragment reads are conflict-free without a
+    // swizzle and a lane's fragments sit at fixed offsets from one base.
+    static constexpr int ROW_P = (NCH + 1) * 16;
+    static constexpr int TILE_P = 32 * ROW_P;            // one 32-codeword tile
     static constexpr int TT = D <= 64 ? 2 : 1;           // 32-token tiles per wave
     static constexpr int WAVES = D <= 64 ? 4 : 8;
     static constexpr int THREADS = 64 * WAVES;
     static constexpr int TOK = WAVES * TT * 32;          // tokens per block
     static constexpr int MIN_BLOCKS = 8 / WAVES;         // two waves per SIMD
-    static constexpr int ROW_BYTES = CPR * 16;
-    static constexpr int BUF_ROW = ROW_BYTES + 16;       // book row + its bias-step A row
-    static constexpr int TILE_BYTES = 32 * ROW_BYTES;    // one 32-codeword tile of a book
     // two book buffers when two full (K = 256) books fit, else one
-    static constexpr int NBUF = 2 * (256 * BUF_ROW + 16) <= kLdsBudget ? 2 : 1;
+    static constexpr int NBUF = 2 * buf_bytes_of(ROW_P, 256) <= kLdsBudget ? 2 : 1;
 };
-
-// Slot of chunk p in LDS row r.  Depends only on the row's place in its
-// 32-row tile (so a lane's fragment offsets are the same in every tile) and
-// makes any aligned 16 rows hit 16 distinct 16-byte bank groups, any aligned
-// 8 rows 8 distinct ones.
-template <int D>
-__device__ __forceinline__ int swz(int r, int p)
-{
-    constexpr int CPR = Cfg<D>::CPR;
-    r &= 31;
-    if (CPR >= 16) return p ^ (r & 15);
-    if (CPR == 8) return p ^ ((r + (r >> 3)) & 7);
-    if (CPR == 4) return p ^ (((r >> 1) + (r >> 3)) & 3);
-    return p ^ (((r >> 2) ^ (r >> 3)) & 1);
-}
-
-// One LDS book buffer: Kp swizzled rows, Kp bias-step A rows, one zero chunk.
-__host__ __device__ constexpr size_t buf_bytes_of(int row_bytes, int Kp)
-{
-    return (size_t)Kp * (row_bytes + 16) + 16;
-}
 
 template <int D>
 size_t lds_bytes(int Kp)
 {
-    return (size_t)Cfg<D>::NBUF * buf_bytes_of(Cfg<D>::ROW_BYTES, Kp);
+    return (size_t)Cfg<D>::NBUF * buf_bytes_of(Cfg<D>::ROW_P, Kp);
 }
 
 // Asynchronously copies stage codebook C ([K][D] fp16) into an LDS buffer of
-// Kp swizzled rows.  Padding slots and rows >= K are loaded from a valid dummy
-// address; their scores are forced to -inf by the bias step.
+// Kp rows.  Each 64-lane copy fills 64 consecutive 16-byte LDS chunks; a
+// row's bias-step slot gets a placeholder (its last data chunk) that
+// book_bias_rows overwrites, and rows >= K are copies of row K-1, so they tie
+// with it and lose to its lower index.
 template <int D>
 __device__ __forceinline__ void book_to_lds_async(const _Float16* __restrict__ C, int K, int Kp,
                                                   uint8_t* buf, int wave, int lane)
 {
-    constexpr int CPR = Cfg<D>::CPR, W = Cfg<D>::WAVES;
-    const int chunks = Kp * CPR;
-    for (int q0 = wave * 64; q0 < chunks; q0 += W * 64) {
-        const int q = q0 + lane;
-        const int r = q / CPR;
-        const int p = swz<D>(r, q % CPR);
-        const _Float16* src = (r < K && p < Cfg<D>::NCH) ? C + (size_t)r * D + p * 8 : C;
+    constexpr int NCH = Cfg<D>::NCH, CH = NCH + 1, STEP = Cfg<D>::WAVES * 64;
+    const int chunks = Kp * CH;   // a multiple of 64 (Kp is)
+    for (int q0 = __builtin_amdgcn_readfirstlane(wave) * 64; q0 < chunks; q0 += STEP) {
+        const uint32_t q = (uint32_t)(q0 + lane);
+        const uint32_t row = q / CH, slot = q - row * CH;
+        const uint32_t off = min(row, (uint32_t)K - 1) * D + min(slot, (uint32_t)NCH - 1) * 8;
+        const _Float16* src = C + off;
         __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)src,
                                          (void __attribute__((address_space(3)))*)(buf + (size_t)q0 * 16),
                                          16, 0, 0);
     }
 }
 
-// Bias-step A rows of a book buffer: (-||c||^2/2 as hi + mid + lo fp16 parts,
-// 1, 2^14, 0, 0, 0); rows >= K start at -inf.
+// Bias-step A chunk of every row: (-||c||^2/2 as hi + mid + lo fp16 parts,
+// 1, 2^14, 0, 0, 0), written into the row's last slot.
 template <int D>
-__device__ __forceinline__ void book_bias_rows(uint8_t* buf, int K, int Kp)
+__device__ __forceinline__ void book_bias_rows(uint8_t* buf, int Kp)
 {
-    half8* arow = (half8*)(buf + (size_t)Kp * Cfg<D>::ROW_BYTES);
+    constexpr int NCH = Cfg<D>::NCH;
     for (int r = threadIdx.x; r < Kp; r += Cfg<D>::THREADS) {
+        uint8_t* row = buf + (size_t)r * Cfg<D>::ROW_P;
         float acc = 0.0f;
 #pragma unroll
-        for (int p = 0; p < Cfg<D>::NCH; ++p) {
-            const half8 v = *(const half8*)(buf + ((size_t)r * Cfg<D>::CPR + swz<D>(r, p)) * 16);
+        for (int p = 0; p < NCH; ++p) {
+            const half8 v = *(const half8*)(row + p * 16);
 #pragma unroll
             for (int e = 0; e < 8; e += 2) {
                 const half2 h = {v[e], v[e + 1]};
@@ -149,12 +137,12 @@ __device__ __forceinline__ void book_bias_rows(uint8_t* buf, int K, int Kp)
         const _Float16 mid = (_Float16)rem;
         const _Float16 lo = (_Float16)(rem - (float)mid);
         half8 a = (half8)(_Float16)0;
-        a[0] = r < K ? hi : (_Float16)(-INFINITY);
-        a[1] = r < K ? mid : (_Float16)0;
-        a[2] = r < K ? lo : (_Float16)0;
+        a[0] = hi;
+        a[1] = mid;
+        a[2] = lo;
         a[3] = (_Float16)1.0f;
         a[4] = (_Float16)kBiasHiScale;
-        arow[r] = a;
+        *(half8*)(row + NCH * 16) = a;
     }
 }
 
@@ -182,42 +170,25 @@ __device__ __forceinline__ void wait_all_and_sync()
 }
 
 // A-operand fragments of one 32-codeword tile: its d/16 data steps and the
-// bias step (a zero chunk for the lanes that hold k = 8..15).
+// bias step.
 template <int D>
 struct Frag {
     half8 a[Cfg<D>::KS];
     half8 bias;
 };
 
-// Per-lane LDS byte offsets of a lane's fragments inside tile 0 of a buffer;
-// tile ct adds ct * TILE_BYTES to the data and ct * bias_step to the bias.
+// A lane's fragments of tile ct start at buf + base + ct * TILE_P, with
+// base = col * ROW_P + 16 hh: data step ks at +32 ks, the bias chunk at
+// +16 NCH.  For the upper half-wave (k = 8..15 of the bias step) that chunk is
+// the next row's first chunk or the buffer's zero pad: finite values that
+// meet the zero half of the token's bias column.
 template <int D>
-struct FragAddr {
-    uint32_t a[Cfg<D>::KS];
-    uint32_t bias;
-    uint32_t bias_step;
-};
-
-template <int D>
-__device__ __forceinline__ FragAddr<D> frag_addr(int Kp, int col, int hh)
+__device__ __forceinline__ void load_frag(Frag<D>& f, const uint8_t* buf, uint32_t base, int ct)
 {
-    FragAddr<D> fa;
+    const uint8_t* tile = buf + base + (size_t)ct * Cfg<D>::TILE_P;
 #pragma unroll
-    for (int ks = 0; ks < Cfg<D>::KS; ++ks)
-        fa.a[ks] = (uint32_t)(col * Cfg<D>::ROW_BYTES + swz<D>(col, 2 * ks + hh) * 16);
-    const uint32_t bias_rows = (uint32_t)(Kp * Cfg<D>::ROW_BYTES);
-    fa.bias = hh == 0 ? bias_rows + (uint32_t)col * 16 : (uint32_t)(Kp * Cfg<D>::BUF_ROW);
-    fa.bias_step = hh == 0 ? 32 * 16 : 0;
-    return fa;
-}
-
-template <int D>
-__device__ __forceinline__ void load_frag(Frag<D>& f, const uint8_t* buf, const FragAddr<D>& fa, int ct)
-{
-    const uint8_t* tile = buf + (size_t)ct * Cfg<D>::TILE_BYTES;
-#pragma unroll
-    for (int ks = 0; ks < Cfg<D>::KS; ++ks) f.a[ks] = *(const half8*)(tile + fa.a[ks]);
-    f.bias = *(const half8*)(buf + fa.bias + (uint32_t)ct * fa.bias_step);
+    for (int ks = 0; ks < Cfg<D>::KS; ++ks) f.a[ks] = *(const half8*)(tile + ks * 32);
+    f.bias = *(const half8*)(tile + Cfg<D>::NCH * 16);
 }
 
 // acc[tt] = bias step + A(tile) x B(tt) over all k-steps; with TWO a second B
@@ -305,7 +276,7 @@ __device__ __forceinline__ void interleave_hint()
 // the fragments of tile ct+2 load and the MFMAs of tile ct+1 run while the
 // argmin of tile ct executes on the VALU.  Tiles 2p and 2p+1 form pair p.
 template <int D, int TT, bool TWO>
-__device__ __forceinline__ void stage_scan(const uint8_t* buf, const FragAddr<D>& fa, int nct,
+__device__ __forceinline__ void stage_scan(const uint8_t* buf, uint32_t fa, int nct,
                                            const half8 (&bz)[TT], const half8 (&bA)[TT][Cfg<D>::KS],
                                            const half8 (&bB)[TT][Cfg<D>::KS], uint32_t (&bkey)[TT],
                                            int (&bpair)[TT])
@@ -345,9 +316,9 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
     using C = Cfg<D>;
     constexpr int KS = C::KS, TT = C::TT, TOK = C::TOK, NBUF = C::NBUF;
     extern __shared__ __align__(16) uint8_t lds[];
-    // LDS: NBUF buffers, each Kp swizzled book rows, Kp bias-step A rows and a
-    // zero chunk; addressed from `lds` so every access stays an LDS access.
-    const size_t buf_bytes = buf_bytes_of(C::ROW_BYTES, Kp);
+    // LDS: NBUF buffers of Kp rows (codeword + bias-step chunk) and a zero
+    // pad; addressed from `lds` so every access stays an LDS access.
+    const size_t buf_bytes = buf_bytes_of(C::ROW_P, Kp);
 
     // XCD-aware order: blocks dispatched to one XCD (every 8th) take consecutive
     // work items, so the blocks of one stream share that XCD's L2 copy of its book.
@@ -389,10 +360,10 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
     }
     const _Float16* bk = books + (int64_t)b * S * K * D;
 
-    // start the first books' copies; zero chunks for the upper half-wave's bias step
+    // start the first books' copies; zero the buffers' end pads
     book_to_lds_async<D>(bk, K, Kp, lds, wave, lane);
     if (NBUF > 1 && S > 1) book_to_lds_async<D>(bk + (size_t)K * D, K, Kp, lds + buf_bytes, wave, lane);
-    if (tid < NBUF) *(half8*)(lds + tid * buf_bytes + (size_t)Kp * C::BUF_ROW) = (half8)(_Float16)0;
+    if (tid < NBUF) *(half8*)(lds + tid * buf_bytes + (size_t)Kp * C::ROW_P) = (half8)(_Float16)0;
 
 #pragma unroll
     for (int tt = 0; tt < TT; ++tt) {
@@ -408,11 +379,11 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
         n2 += __shfl_xor(n2, 32);
         bz[tt] = bias_column(0.5f * n2 * (1.0f + 0x1p-10f), hh);
     }
-    const FragAddr<D> fa = frag_addr<D>(Kp, col, hh);
+    const uint32_t fa = (uint32_t)(col * C::ROW_P + hh * 16);
 
     wait_all_and_sync();
-    book_bias_rows<D>(lds, K, Kp);
-    if (NBUF > 1 && S > 1) book_bias_rows<D>(lds + buf_bytes, K, Kp);
+    book_bias_rows<D>(lds, Kp);
+    if (NBUF > 1 && S > 1) book_bias_rows<D>(lds + buf_bytes, Kp);
     __syncthreads();
 
     const int nct = Kp / 32;  // even
@@ -448,9 +419,9 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
             bz[tt] = bias_column(-__uint_as_float(val) * (1.0f + 0x1p-10f), hh);
             // this lane's chunks of the chosen codeword
             half8 cv[KS];
-            const uint8_t* crow = buf + (size_t)cw * C::ROW_BYTES;
+            const uint8_t* crow = buf + (size_t)cw * C::ROW_P + hh * 16;
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) cv[ks] = *(const half8*)(crow + swz<D>(cw, 2 * ks + hh) * 16);
+            for (int ks = 0; ks < KS; ++ks) cv[ks] = *(const half8*)(crow + ks * 32);
             const bool last = st + 1 == S;
             if (HILO && st >= 1 && !last) {
                 // r = (hi + lo) - c for st >= 2, (x - c_0) - c_1 for st == 1; split again
@@ -494,7 +465,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
             } else if (st + 2 < S) {
                 book_to_lds_async<D>(bk + (size_t)(st + 2) * K * D, K, Kp, lds + cur * buf_bytes, wave, lane);
             }
-            if (NBUF == 1 || st >= 1) book_bias_rows<D>(lds + (NBUF > 1 ? ((st + 1) & 1) : 0) * buf_bytes, K, Kp);
+            if (NBUF == 1 || st >= 1) book_bias_rows<D>(lds + (NBUF > 1 ? ((st + 1) & 1) : 0) * buf_bytes, Kp);
             __syncthreads();
         }
     }
