@@ -148,18 +148,26 @@ __global__ __launch_bounds__(kBlock) void cgr_encode_kernel(
     const int N = cd.N, L = cd.L;
     // LDS: the 256-entry vertex table (entries >= N are NaN, so a symbol
     // outside the alphabet yields a NaN point), then the symbol tile.
+    static_assert(kBlock == 256, "one vertex entry per thread");
     double2* V = (double2*)lds;
     uint8_t* tile = lds + 256 * sizeof(double2);
-    for (int c = threadIdx.x; c < 256; c += blockDim.x)
-        V[c] = c < N ? ((const double2*)(gtab + table_off_V(N)))[c] : make_double2(NAN, NAN);
+    // This thread's vertex entry: loaded first, stored once the first tile's
+    // symbol loads are in flight, so the two memory latencies overlap.
+    const double2 vreg = (int)threadIdx.x < N ? ((const double2*)(gtab + table_off_V(N)))[threadIdx.x]
+                                              : make_double2(NAN, NAN);
+    bool staged = false;
     for (int64_t tl = blockIdx.x; tl < n_tiles; tl += gridDim.x) {
         const int64_t s = tl / tiles_per_stream;
         const int64_t j0 = (tl - s * tiles_per_stream) * kBlock;
         const int64_t nsp = min((int64_t)kBlock, n_spans - j0);
         const int64_t g0 = s * n_sym + j0 * L;
         const int64_t g1 = s * n_sym + min(n_sym, (j0 + nsp) * L);
-        __syncthreads();  // tables staged / previous tile consumed
+        __syncthreads();  // previous tile consumed
         bytes_to_lds(sym, g0, g1, tile);
+        if (!staged) {
+            V[threadIdx.x] = vreg;
+            staged = true;
+        }
         __syncthreads();
         if (threadIdx.x < nsp) {
             const int64_t a = (j0 + threadIdx.x) * L;
@@ -182,6 +190,14 @@ __global__ __launch_bounds__(kBlock) void cgr_decode_kernel(
 {
     extern __shared__ __align__(16) uint8_t lds[];
     const int N = cd.N, L = cd.L;
+    // The first tile's point is loaded before the tables are staged, so the
+    // two memory latencies overlap.
+    double2 P0 = make_double2(0.0, 0.0);
+    if ((int64_t)blockIdx.x < n_tiles) {
+        const int64_t s = (int64_t)blockIdx.x / tiles_per_stream;
+        const int64_t j0 = ((int64_t)blockIdx.x - s * tiles_per_stream) * kBlock;
+        if ((int64_t)threadIdx.x < min((int64_t)kBlock, n_spans - j0)) P0 = pts[s * n_spans + j0 + threadIdx.x];
+    }
     Tables t = stage_tables(gtab, N, lds, VERIFY, EXACT);
     uint8_t* tile = lds + table_bytes(N);
     for (int64_t tl = blockIdx.x; tl < n_tiles; tl += gridDim.x) {
@@ -196,7 +212,7 @@ __global__ __launch_bounds__(kBlock) void cgr_decode_kernel(
             const int64_t a = (j0 + threadIdx.x) * L;
             const int len = (int)min((int64_t)L, n_sym - a);
             uint8_t* my = tile + (g0 & 3) + threadIdx.x * L;
-            const double2 P = pts[s * n_spans + j0 + threadIdx.x];
+            const double2 P = tl == (int64_t)blockIdx.x ? P0 : pts[s * n_spans + j0 + threadIdx.x];
             double qx = P.x, qy = P.y;
             for (int k = len - 1; k >= 0; --k) {
                 const int c = sector_of<EXACT>(qx, qy, t, N);
@@ -230,18 +246,28 @@ __global__ __launch_bounds__(kBlock) void span_lookup_kernel(
 {
     extern __shared__ __align__(16) uint8_t lds[];
     const int N = cd.N, L = cd.L;
-    Tables t = stage_tables(gtab, N, lds, false, EXACT);
-    __syncthreads();
     const int64_t n_tok = n_sym / S;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     const int64_t n_iter = (n_q + stride - 1) / stride;  // same trip count for every lane
+    // The first query and the point of its first span are loaded before the
+    // tables are staged, so the memory latencies overlap.
+    const int64_t q0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    int64_t s0 = 0, tk0 = 0;
+    double2 P0 = make_double2(0.0, 0.0);
+    if (q0 < n_q) {
+        s0 = q_stream[q0];
+        tk0 = q_token[q0];
+        if (s0 < n_streams && tk0 < n_tok) P0 = pts[s0 * n_spans + tk0 * S / L];
+    }
+    Tables t = stage_tables(gtab, N, lds, false, EXACT);
+    __syncthreads();
     for (int64_t it = 0; it < n_iter; ++it) {
-        const int64_t q = it * stride + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+        const int64_t q = it * stride + q0;
         int status = 0;
         uint64_t got = 0;
         if (q < n_q) {
-            const int64_t s = q_stream[q];
-            const int64_t tk = q_token[q];
+            const int64_t s = it == 0 ? s0 : (int64_t)q_stream[q];
+            const int64_t tk = it == 0 ? tk0 : (int64_t)q_token[q];
             if (s >= n_streams || tk >= n_tok) {
                 status = 2;
             } else {
@@ -250,7 +276,7 @@ __global__ __launch_bounds__(kBlock) void span_lookup_kernel(
                 for (int64_t j = j0; j <= j1; ++j) {
                     const int64_t b = j * L;
                     const int len = (int)min((int64_t)L, n_sym - b);
-                    const double2 P = pts[s * n_spans + j];
+                    const double2 P = (it == 0 && j == j0) ? P0 : pts[s * n_spans + j];
                     double qx = P.x, qy = P.y;
                     for (int k = len - 1; k >= 0; --k) {
                         const int c = sector_of<EXACT>(qx, qy, t, N);

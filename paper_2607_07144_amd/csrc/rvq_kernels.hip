@@ -113,37 +113,52 @@ __device__ __forceinline__ void book_to_lds_async(const _Float16* __restrict__ C
     }
 }
 
-// Bias-step A chunk of every row: (-||c||^2/2 as hi + mid + lo fp16 parts,
-// 1, 2^14, 0, 0, 0), written into the row's last slot.
-template <int D>
-__device__ __forceinline__ void book_bias_rows(uint8_t* buf, int Kp)
+// Bias-step A chunk of every row of NB buffers: (-||c||^2/2 as hi + mid + lo
+// fp16 parts, 1, 2^14, 0, 0, 0), written into the row's last slot.  All rows'
+// LDS reads are issued before any norm is formed, so their latencies overlap.
+template <int D, int NB>
+__device__ __forceinline__ void book_bias_rows(uint8_t* buf0, uint8_t* buf1, int Kp)
 {
     constexpr int NCH = Cfg<D>::NCH;
     for (int r = threadIdx.x; r < Kp; r += Cfg<D>::THREADS) {
-        uint8_t* row = buf + (size_t)r * Cfg<D>::ROW_P;
-        float acc = 0.0f;
+        uint8_t* row[2] = {buf0 + (size_t)r * Cfg<D>::ROW_P, buf1 + (size_t)r * Cfg<D>::ROW_P};
+        half8 v[NB][NCH];
 #pragma unroll
-        for (int p = 0; p < NCH; ++p) {
-            const half8 v = *(const half8*)(row + p * 16);
+        for (int b = 0; b < NB; ++b)
 #pragma unroll
-            for (int e = 0; e < 8; e += 2) {
-                const half2 h = {v[e], v[e + 1]};
-                acc = __builtin_amdgcn_fdot2(h, h, acc, false);
+            for (int p = 0; p < NCH; ++p) v[b][p] = *(const half8*)(row[b] + p * 16);
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            float acc = 0.0f;
+#pragma unroll
+            for (int p = 0; p < NCH; ++p) {
+#pragma unroll
+                for (int e = 0; e < 8; e += 2) {
+                    const half2 h = {v[b][p][e], v[b][p][e + 1]};
+                    acc = __builtin_amdgcn_fdot2(h, h, acc, false);
+                }
             }
+            const float n = -0.5f * acc;
+            const _Float16 hi = (_Float16)n;
+            const float rem = n - (float)hi;
+            const _Float16 mid = (_Float16)rem;
+            const _Float16 lo = (_Float16)(rem - (float)mid);
+            half8 a = (half8)(_Float16)0;
+            a[0] = hi;
+            a[1] = mid;
+            a[2] = lo;
+            a[3] = (_Float16)1.0f;
+            a[4] = (_Float16)kBiasHiScale;
+            *(half8*)(row[b] + NCH * 16) = a;
         }
-        const float n = -0.5f * acc;
-        const _Float16 hi = (_Float16)n;
-        const float rem = n - (float)hi;
-        const _Float16 mid = (_Float16)rem;
-        const _Float16 lo = (_Float16)(rem - (float)mid);
-        half8 a = (half8)(_Float16)0;
-        a[0] = hi;
-        a[1] = mid;
-        a[2] = lo;
-        a[3] = (_Float16)1.0f;
-        a[4] = (_Float16)kBiasHiScale;
-        *(half8*)(row + NCH * 16) = a;
     }
+}
+
+// The value lane l ^ 32 holds (hh: this lane's half-wave).
+__device__ __forceinline__ uint32_t lane_xor32(uint32_t v, int hh)
+{
+    const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    return hh ? r[0] : r[1];
 }
 
 // Bias-step B column of a token: slots 0-2 multiply the norm parts (1, 1, 1),
@@ -376,14 +391,16 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
                 n2 = __builtin_amdgcn_fdot2(h, h, n2, false);
             }
         }
-        n2 += __shfl_xor(n2, 32);
+        n2 += __uint_as_float(lane_xor32(__float_as_uint(n2), hh));
         bz[tt] = bias_column(0.5f * n2 * (1.0f + 0x1p-10f), hh);
     }
     const uint32_t fa = (uint32_t)(col * C::ROW_P + hh * 16);
 
     wait_all_and_sync();
-    book_bias_rows<D>(lds, Kp);
-    if (NBUF > 1 && S > 1) book_bias_rows<D>(lds + buf_bytes, Kp);
+    if (NBUF > 1 && S > 1)
+        book_bias_rows<D, 2>(lds, lds + buf_bytes, Kp);
+    else
+        book_bias_rows<D, 1>(lds, lds, Kp);
     __syncthreads();
 
     const int nct = Kp / 32;  // even
@@ -408,8 +425,8 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
             int cw = (2 * bpair[tt] + (li >> 4)) * 32 + 8 * ((li & 15) >> 2) + 4 * hh + (li & 3);
             cw = min(cw, K - 1);  // only reachable with all-NaN scores; keeps reads in bounds
             uint32_t val = bkey[tt] & ~31u;
-            const uint32_t oval = __shfl_xor(val, 32);
-            const int ocw = __shfl_xor(cw, 32);
+            const uint32_t oval = lane_xor32(val, hh);
+            const int ocw = (int)lane_xor32((uint32_t)cw, hh);
             if (oval < val || (oval == val && ocw < cw)) {
                 val = oval;
                 cw = ocw;
@@ -465,7 +482,10 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
             } else if (st + 2 < S) {
                 book_to_lds_async<D>(bk + (size_t)(st + 2) * K * D, K, Kp, lds + cur * buf_bytes, wave, lane);
             }
-            if (NBUF == 1 || st >= 1) book_bias_rows<D>(lds + (NBUF > 1 ? ((st + 1) & 1) : 0) * buf_bytes, Kp);
+            if (NBUF == 1 || st >= 1) {
+                uint8_t* nb = lds + (NBUF > 1 ? ((st + 1) & 1) : 0) * buf_bytes;
+                book_bias_rows<D, 1>(nb, nb, Kp);
+            }
             __syncthreads();
         }
     }
