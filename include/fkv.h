@@ -157,6 +157,42 @@ int fkv_span_lookup(const fkv_codec* c, const void* dev_table, const double* poi
                     const uint32_t* q_token, int64_t n_q, uint8_t* out, uint8_t* q_status,
                     uint32_t* n_failed, void* stream);
 
+/* ---- rehydrate: reconstruction of archived positions (Sec. 3 "Setup": an
+ * archived position is replaced by the sum of its codewords; Sec. 5: matched
+ * positions are rehydrated from the archive alone) ---------------------------
+ * For query q with (s, t) = (q_stream[q], q_token[q]): the token's S symbols
+ * i_0..i_{S-1} are read back by random access (as fkv_span_lookup), then
+ *     out[q][e] = sum_{st<S} C[b][st][i_st][e],   b = stream_book[s],
+ * formed exactly and rounded once to binary16 (round to nearest, ties to
+ * even).
+ *   books_f16    device binary16 [n_books][S][K][d], 16-byte aligned
+ *   stream_book  device int32 [n_streams]
+ *   K, d         codewords per stage (1..256); head dim (multiple of 8, 8..256)
+ *   out_f16      device binary16 [n_q][d], 16-byte aligned
+ *   q_status     device u8 [n_q], nullable: 0 ok, 1 a decoded span failed its
+ *                anchor check, 2 out of range, 3 invalid book id or a decoded
+ *                symbol >= K; the out row is zero unless the status is 0
+ *   n_failed     device u32 counter, += number of queries with status != 0;
+ *                nullable */
+int fkv_rehydrate(const fkv_codec* c, const void* dev_table, const double* points, int64_t n_streams,
+                  int64_t n_sym, int32_t S, const uint16_t* books_f16, const int32_t* stream_book,
+                  int32_t n_books, int32_t K, int32_t d, const uint32_t* q_stream,
+                  const uint32_t* q_token, int64_t n_q, uint16_t* out_f16, uint8_t* q_status,
+                  uint32_t* n_failed, void* stream);
+
+/* ---- append (Sec. 2 and Table 1, "append") ---------------------------------
+ * Extends each of n_streams streams of n_old symbols by m symbols
+ * (sym_new [n_streams][m], device u8), re-walking only from the stream's last
+ * stored point: a partial last span continues from points[s][n_old / L], a
+ * span that starts at a multiple of L starts from the anchor (0,0), and the
+ * point of every span the new symbols fall in is written back.  points is
+ * [n_streams][cap_spans][2] (device f64, 16-byte aligned) with
+ * cap_spans >= ceil((n_old + m) / L); spans before the open one are not
+ * touched.  The result is bit-identical to fkv_cgr_encode_spans of the whole
+ * stream.  A symbol >= N makes its span's point NaN. */
+int fkv_cgr_append(const fkv_codec* c, const void* dev_table, double* points, int64_t cap_spans,
+                   int64_t n_streams, int64_t n_old, const uint8_t* sym_new, int64_t m, void* stream);
+
 /* Static description of a status code. */
 const char* fkv_status_string(int status);
 

@@ -64,6 +64,11 @@ def _load():
     lib.fkvo_rvq_assign.argtypes = [c_i64, c_i64, c_i64, c_i64, c_i32, c_i32, c_i32, c_p, c_p, c_p,
                                     c_p, c_p, c_p, c_p, c_dbl, c_p, c_i32]
     lib.fkvo_rvq_assign.restype = None
+    lib.fkvo_rehydrate.argtypes = [c_i32, c_dbl, c_i32, c_p, c_p, c_p, c_i64, c_i64, c_i32, c_p, c_p,
+                                   c_i32, c_i32, c_i32, c_p, c_p, c_i64, c_p, c_p, c_i32]
+    lib.fkvo_rehydrate.restype = c_i64
+    lib.fkvo_append.argtypes = [c_i32, c_dbl, c_i32, c_p, c_p, c_i64, c_i64, c_i64, c_p, c_i64, c_i32]
+    lib.fkvo_append.restype = None
     _lib = lib
     return lib
 
@@ -193,3 +198,49 @@ def rvq_assign(x_f16: np.ndarray, books_f16: np.ndarray, stream_book: np.ndarray
                             _ptr(fz), float(force_tol), _ptr(counts), threads or default_threads())
     return {"symbols": sym, "residual": res, "gaps": gaps, "n_forced": int(counts[0]),
             "n_hard": int(counts[1])}
+
+
+def rehydrate(codec: Codec, points: np.ndarray, n_sym: int, S: int, books_f16: np.ndarray,
+              stream_book: np.ndarray, q_stream: np.ndarray, q_token: np.ndarray,
+              threads: int | None = None):
+    """Reconstruction of archived positions from the archive alone (Sec. 3 "Setup", Sec. 5).
+
+    -> (out f64 [n_q][d]: exact sum of the S codewords, status u8 [n_q], n_failed).
+    Status 0 ok, 1 anchor failure, 2 out of range, 3 invalid book or symbol >= K."""
+    if codec.L > 64:
+        raise ValueError("oracle lookup supports L <= 64")
+    pts = np.ascontiguousarray(points, dtype=np.float64)
+    bk = np.ascontiguousarray(books_f16, dtype=np.float16)
+    nb, S2, K, d = bk.shape
+    assert S2 == S
+    sb = np.ascontiguousarray(stream_book, dtype=np.int32)
+    assert sb.shape == (pts.shape[0],)
+    qs = np.ascontiguousarray(q_stream, dtype=np.uint32)
+    qt = np.ascontiguousarray(q_token, dtype=np.uint32)
+    nq = qs.shape[0]
+    out = np.zeros((nq, d), np.float64)
+    st = np.zeros(nq, np.uint8)
+    nf = _load().fkvo_rehydrate(codec.N, codec.r, codec.L, _ptr(codec.V), _ptr(codec.W), _ptr(pts),
+                                pts.shape[0], n_sym, S, _ptr(bk.view(np.uint16)), _ptr(sb), nb, K, d,
+                                _ptr(qs), _ptr(qt), nq, _ptr(out), _ptr(st), threads or default_threads())
+    return out, st, int(nf)
+
+
+def append(codec: Codec, points: np.ndarray, n_old: int, sym_new: np.ndarray,
+           threads: int | None = None) -> np.ndarray:
+    """Append (Sec. 2, Table 1): extend every stream of n_old symbols by sym_new
+    [n_streams][m], re-walking only from the last stored point.  points
+    [n_streams][cap_spans][2] (cap_spans >= ceil((n_old + m) / L)) is updated in a
+    copy, which is returned."""
+    pts = np.array(points, dtype=np.float64, copy=True, order="C")
+    sym = np.ascontiguousarray(sym_new, dtype=np.uint8)
+    ns, cap = pts.shape[0], pts.shape[1]
+    assert sym.shape[0] == ns
+    m = sym.shape[1]
+    if codec.n_spans(n_old + m) > cap:
+        raise ValueError("points capacity too small")
+    if m and int(sym.max()) >= codec.N:
+        raise ValueError("symbol out of alphabet")
+    _load().fkvo_append(codec.N, codec.r, codec.L, _ptr(codec.V), _ptr(pts), cap, ns, n_old, _ptr(sym),
+                        m, threads or default_threads())
+    return pts

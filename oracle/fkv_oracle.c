@@ -345,3 +345,94 @@ void fkvo_rvq_assign(int64_t n_streams, int64_t T, int64_t t_begin, int64_t t_en
         counts[1] = n_hard;
     }
 }
+
+/* ------------------------------------------------------------- rehydrate -- */
+
+/*
+ * Sec. 3 ("Setup"): an archived position's K or V vector is replaced by the sum
+ * of its S codewords; Sec. 5: a matched position is rehydrated from the
+ * archive alone.  Query q = (stream, token): its S symbols are read back by
+ * random access (fkvo_span_lookup's steps), then
+ *     out[q][e] = sum_{st=0..S-1} C[b][st][i_st][e],   b = stream_book[stream],
+ * summed in fp64 in stage order (exact: a few binary16 values).
+ * q_status: 0 ok, 1 a decoded span failed its anchor check, 2 out of range,
+ * 3 invalid book id or a decoded symbol >= K; out row is zero unless 0.
+ */
+int64_t fkvo_rehydrate(int32_t N, double r, int32_t L, const double* V, const double* W,
+                       const double* points, int64_t n_streams, int64_t n_sym, int32_t S,
+                       const uint16_t* books, const int32_t* stream_book, int32_t n_books,
+                       int32_t K, int32_t d, const uint32_t* q_stream, const uint32_t* q_token,
+                       int64_t n_q, double* out, uint8_t* q_status, int32_t threads)
+{
+    uint8_t* sym = (uint8_t*)malloc((size_t)(n_q > 0 ? n_q : 1) * (size_t)S);
+    uint8_t* st = (uint8_t*)malloc((size_t)(n_q > 0 ? n_q : 1));
+    fkvo_span_lookup(N, r, L, V, W, points, n_streams, n_sym, S, q_stream, q_token, n_q, sym, st,
+                     threads);
+    int64_t failed = 0;
+#pragma omp parallel for schedule(static) num_threads(threads) reduction(+ : failed)
+    for (int64_t q = 0; q < n_q; ++q) {
+        uint8_t s_ = st[q];
+        int32_t b = 0;
+        if (s_ == 0) {
+            b = stream_book[q_stream[q]];
+            if (b < 0 || b >= n_books) s_ = 3;
+            for (int32_t k = 0; k < S; ++k)
+                if (sym[q * S + k] >= K) s_ = 3;
+        }
+        for (int32_t e = 0; e < d; ++e) {
+            double acc = 0.0;
+            if (s_ == 0)
+                for (int32_t k = 0; k < S; ++k) {
+                    const uint16_t* row = books + (((int64_t)b * S + k) * K + sym[q * S + k]) * d;
+                    acc = acc + fkvo_half_to_double(row[e]);
+                }
+            out[q * d + e] = acc;
+        }
+        if (q_status) q_status[q] = s_;
+        if (s_) failed += 1;
+    }
+    free(sym);
+    free(st);
+    return failed;
+}
+
+/* ---------------------------------------------------------------- append -- */
+
+/*
+ * Sec. 2 / Table 1 (append): new symbols extend a stream by re-walking only
+ * from its last stored point.  Each of n_streams streams holds n_old symbols
+ * whose span points sit in points[s][0..][2] (capacity cap_spans spans per
+ * stream).  m new symbols per stream (sym_new[s][0..m)) are appended: a partial
+ * last span continues from its stored point, every span that starts at a
+ * multiple of L starts from the anchor (0,0), and each touched span's point is
+ * written back.  The result equals a bulk encode of the whole stream.
+ */
+void fkvo_append(int32_t N, double r, int32_t L, const double* V, double* points,
+                 int64_t cap_spans, int64_t n_streams, int64_t n_old, const uint8_t* sym_new,
+                 int64_t m, int32_t threads)
+{
+#pragma omp parallel for schedule(static) num_threads(threads)
+    for (int64_t s = 0; s < n_streams; ++s) {
+        double* P = points + s * cap_spans * 2;
+        double px = 0.0, py = 0.0;
+        if (n_old % L != 0) {
+            px = P[(n_old / L) * 2];
+            py = P[(n_old / L) * 2 + 1];
+        }
+        for (int64_t k = 0; k < m; ++k) {
+            int64_t pos = n_old + k;
+            if (pos % L == 0) {
+                px = 0.0;
+                py = 0.0;
+            }
+            int32_t c = sym_new[s * m + k];
+            double vx = c < N ? V[2 * c] : NAN, vy = c < N ? V[2 * c + 1] : NAN;
+            double tx = px - vx, ty = py - vy;
+            double ux = r * tx, uy = r * ty;
+            px = vx + ux;
+            py = vy + uy;
+            P[(pos / L) * 2] = px;
+            P[(pos / L) * 2 + 1] = py;
+        }
+    }
+}

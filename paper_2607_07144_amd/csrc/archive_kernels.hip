@@ -1,0 +1,198 @@
+// archive_kernels.hip -- reading reconstructions out of the archive and
+// appending to it, for gfx950.
+//
+// Rehydrate (Sec. 3 "Setup": an archived position's K/V vector is replaced by
+// the sum of its S codewords; Sec. 5: a matched position is rehydrated from the
+// archive alone): random access to the token's S symbols (one query per lane,
+// as in span lookup), then a block-cooperative gather of the codeword rows --
+// consecutive lanes take consecutive 16-byte chunks of one output row, so the
+// codeword reads and the output writes are contiguous runs.  The S codewords
+// are summed in fp64 (exact for a few binary16 values) and rounded once to
+// binary16, so the result is the correctly rounded reconstruction.
+//
+// Append (Sec. 2, Table 1): one stream per lane re-walks from its last stored
+// point; a span that starts at a multiple of L starts from the anchor (0,0).
+// The forward step is the bulk encoder's, operation for operation, so the
+// points equal a bulk encode of the whole stream bit for bit.
+#include "cgr_device.h"
+
+namespace fkv {
+namespace {
+
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+
+// Correctly rounded binary64 -> binary16 (round to nearest, ties to even): the
+// conversion to binary32 is made round-to-odd (truncate, then set the last
+// bit when inexact), which carries enough information for the final
+// round-to-nearest-even step to binary16 (binary32 has 13 more bits).
+__device__ inline _Float16 f64_to_f16(double v)
+{
+    const float f = (float)v;
+    uint32_t u = __float_as_uint(f);
+    if ((double)f != v) {
+        if (fabs((double)f) > fabs(v)) u -= 1;   // towards zero
+        u |= 1u;
+    }
+    return (_Float16)__uint_as_float(u);
+}
+
+// ---------------------------------------------------------------- rehydrate --
+
+template <bool EXACT>
+__global__ __launch_bounds__(kBlock) void rehydrate_kernel(
+    const double2* __restrict__ pts, const uint32_t* __restrict__ q_stream,
+    const uint32_t* __restrict__ q_token, const _Float16* __restrict__ books,
+    const int32_t* __restrict__ stream_book, _Float16* __restrict__ out, uint8_t* __restrict__ q_status,
+    uint32_t* __restrict__ n_failed, const uint8_t* __restrict__ gtab, CodecArgs cd, int64_t n_streams,
+    int64_t n_sym, int64_t n_spans, int S, int K, int d, int n_books, int64_t n_q)
+{
+    extern __shared__ __align__(16) uint8_t lds[];
+    const int N = cd.N;
+    Tables t = stage_tables(gtab, N, lds, false, EXACT);
+    // After the tables: each query of the current batch's book id (-1: no
+    // output) and its packed symbols.
+    int32_t* qbook = (int32_t*)(lds + table_bytes(N));
+    uint64_t* qsym = (uint64_t*)(lds + table_bytes(N) + kBlock * sizeof(int32_t));
+    __syncthreads();
+    const int64_t n_tok = n_sym / S;
+    const int nch = d / 8;   // 16-byte chunks per output row
+    for (int64_t base = (int64_t)blockIdx.x * kBlock; base < n_q; base += (int64_t)gridDim.x * kBlock) {
+        const int64_t q = base + threadIdx.x;
+        int status = 0;
+        uint64_t got = 0;
+        int32_t b = -1;
+        if (q < n_q) {
+            const int64_t s = q_stream[q];
+            const int64_t tk = q_token[q];
+            if (s >= n_streams || tk >= n_tok) {
+                status = 2;
+            } else {
+                status = lookup_token<EXACT>(pts, t, cd, s, tk, S, n_sym, n_spans, false,
+                                             make_double2(0.0, 0.0), &got);
+                if (status == 0) {
+                    b = stream_book[s];
+                    if (b < 0 || b >= n_books) status = 3;
+                    for (int k = 0; k < S; ++k)
+                        if ((int)((got >> (8 * k)) & 0xff) >= K) status = 3;
+                }
+            }
+            if (q_status) q_status[q] = (uint8_t)status;
+        }
+        count_flags(status != 0, n_failed);
+        qbook[threadIdx.x] = status == 0 ? b : -1;
+        qsym[threadIdx.x] = got;
+        __syncthreads();
+        const int nq = (int)min((int64_t)kBlock, n_q - base);
+        for (int task = threadIdx.x; task < nq * nch; task += kBlock) {
+            const int ql = task / nch, ch = task - ql * nch;
+            const int32_t bb = qbook[ql];
+            const uint64_t sy = qsym[ql];
+            double acc[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc[e] = 0.0;
+            if (bb >= 0) {
+                for (int k = 0; k < S; ++k) {
+                    const int i = (int)((sy >> (8 * k)) & 0xff);
+                    const half8 v = *(const half8*)(books + (((int64_t)bb * S + k) * K + i) * d + ch * 8);
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) acc[e] = acc[e] + (double)v[e];
+                }
+            }
+            half8 o;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) o[e] = f64_to_f16(acc[e]);
+            *(half8*)(out + (base + ql) * d + ch * 8) = o;
+        }
+        __syncthreads();   // the batch's query table is consumed
+    }
+}
+
+// ------------------------------------------------------------------- append --
+
+__global__ __launch_bounds__(kBlock) void append_kernel(double2* __restrict__ pts,
+                                                         const uint8_t* __restrict__ sym_new,
+                                                         const uint8_t* __restrict__ gtab, CodecArgs cd,
+                                                         int64_t cap_spans, int64_t n_streams, int64_t n_old,
+                                                         int64_t m)
+{
+    __shared__ double2 V[256];   // entries >= N are NaN: a symbol outside the alphabet gives NaN
+    const int N = cd.N, L = cd.L;
+    V[threadIdx.x] = (int)threadIdx.x < N ? ((const double2*)(gtab + table_off_V(N)))[threadIdx.x]
+                                          : make_double2(NAN, NAN);
+    __syncthreads();
+    for (int64_t s = (int64_t)blockIdx.x * kBlock + threadIdx.x; s < n_streams;
+         s += (int64_t)gridDim.x * kBlock) {
+        double2* P = pts + s * cap_spans;
+        double px = 0.0, py = 0.0;
+        if (n_old % L != 0) {
+            const double2 p = P[n_old / L];
+            px = p.x;
+            py = p.y;
+        }
+        const uint8_t* my = sym_new + s * m;
+        for (int64_t k = 0; k < m; ++k) {
+            const int64_t pos = n_old + k;
+            if (pos % L == 0) {
+                px = 0.0;
+                py = 0.0;
+            }
+            encode_step(px, py, V[my[k]], cd.r);
+            if ((pos + 1) % L == 0 || k == m - 1) P[pos / L] = make_double2(px, py);
+        }
+    }
+}
+
+}  // namespace
+}  // namespace fkv
+
+using namespace fkv;
+
+extern "C" int fkv_rehydrate(const fkv_codec* c, const void* dev_table, const double* points,
+                             int64_t n_streams, int64_t n_sym, int32_t S, const uint16_t* books_f16,
+                             const int32_t* stream_book, int32_t n_books, int32_t K, int32_t d,
+                             const uint32_t* q_stream, const uint32_t* q_token, int64_t n_q,
+                             uint16_t* out_f16, uint8_t* q_status, uint32_t* n_failed, void* stream)
+{
+    if (!codec_ok(c) || !dev_table || n_streams < 0 || n_sym < 0 || n_q < 0) return FKV_ERR_INVALID_ARG;
+    if (S < 1 || S > 8 || n_sym % S != 0) return FKV_ERR_INVALID_ARG;
+    if (n_books < 1 || K < 1 || K > 256 || d < 8 || d > 256 || d % 8 != 0) return FKV_ERR_INVALID_ARG;
+    if (n_q == 0) return FKV_OK;
+    if (!q_stream || !q_token || !out_f16 || !books_f16 || !aligned(dev_table, 16)) return FKV_ERR_INVALID_ARG;
+    if (n_streams > 0 && n_sym > 0 && (!points || !aligned(points, 16) || !stream_book))
+        return FKV_ERR_INVALID_ARG;
+    if (!aligned(books_f16, 16) || !aligned(out_f16, 16) || !aligned(q_stream, 4) || !aligned(q_token, 4))
+        return FKV_ERR_INVALID_ARG;
+    if ((stream_book && !aligned(stream_book, 4)) || (n_failed && !aligned(n_failed, 4)))
+        return FKV_ERR_INVALID_ARG;
+    const int64_t n_spans = (n_sym + c->L - 1) / c->L;
+    const size_t shm = table_bytes(c->N) + (size_t)kBlock * (sizeof(int32_t) + sizeof(uint64_t));
+    const int64_t nb = blocks_for((n_q + kBlock - 1) / kBlock);
+    const hipStream_t st = (hipStream_t)stream;
+    if (needs_exact_sectors(c))
+        hipLaunchKernelGGL((rehydrate_kernel<true>), dim3((unsigned)nb), dim3(kBlock), shm, st,
+                           (const double2*)points, q_stream, q_token, (const _Float16*)books_f16, stream_book,
+                           (_Float16*)out_f16, q_status, n_failed, (const uint8_t*)dev_table, codec_args(c),
+                           n_streams, n_sym, n_spans, S, K, d, n_books, n_q);
+    else
+        hipLaunchKernelGGL((rehydrate_kernel<false>), dim3((unsigned)nb), dim3(kBlock), shm, st,
+                           (const double2*)points, q_stream, q_token, (const _Float16*)books_f16, stream_book,
+                           (_Float16*)out_f16, q_status, n_failed, (const uint8_t*)dev_table, codec_args(c),
+                           n_streams, n_sym, n_spans, S, K, d, n_books, n_q);
+    return launch_status();
+}
+
+extern "C" int fkv_cgr_append(const fkv_codec* c, const void* dev_table, double* points, int64_t cap_spans,
+                              int64_t n_streams, int64_t n_old, const uint8_t* sym_new, int64_t m,
+                              void* stream)
+{
+    if (!codec_ok(c) || !dev_table || cap_spans < 0 || n_streams < 0 || n_old < 0 || m < 0)
+        return FKV_ERR_INVALID_ARG;
+    if ((n_old + m + c->L - 1) / c->L > cap_spans) return FKV_ERR_INVALID_ARG;
+    if (n_streams == 0 || m == 0) return FKV_OK;
+    if (!points || !sym_new || !aligned(points, 16) || !aligned(dev_table, 16)) return FKV_ERR_INVALID_ARG;
+    const int64_t nb = blocks_for((n_streams + kBlock - 1) / kBlock);
+    hipLaunchKernelGGL(append_kernel, dim3((unsigned)nb), dim3(kBlock), 0, (hipStream_t)stream,
+                       (double2*)points, sym_new, (const uint8_t*)dev_table, codec_args(c), cap_spans, n_streams,
+                       n_old, m);
+    return launch_status();
+}

@@ -1,0 +1,194 @@
+// cgr_device.h -- codec helpers shared by the span kernels (encode, decode,
+// lookup, rehydrate, append): per-alphabet tables in LDS, the forward step,
+// the cell (sector) of a point, the inverse step, the anchor check, random
+// access to one token's symbols, and the host-side launch helpers.
+//
+// Floating point: the forward step must be bit-reproducible, so every file
+// including this header is compiled without FP contraction; fused
+// multiply-adds appear only where written explicitly (the inverse map, whose
+// points are never compared -- only the symbols they yield).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "fkv.h"
+#include "fkv_hip_common.h"
+#include "fkv_internal.h"
+
+#pragma clang fp contract(off)
+
+namespace fkv {
+namespace {
+
+constexpr int kBlock = 256;        // threads per block = spans per tile
+constexpr int kMaxBlocks = 2048;   // persistent grid cap (8 blocks per CU)
+
+struct CodecArgs {
+    int N;
+    int L;
+    double r;
+    double inv_r;
+};
+
+// LDS image of the device table, sized for the alphabet.
+struct Tables {
+    double2* V;
+    double2* W;
+    double2* Wr;
+    LutEntry* lut;
+};
+
+// Copies the needed sections of the device table into LDS at the same
+// offsets (sections not needed are left unwritten).
+__device__ inline Tables stage_tables(const uint8_t* __restrict__ gtab, int N, uint8_t* lds,
+                                      bool needV, bool needW)
+{
+    Tables t;
+    t.V = (double2*)(lds + table_off_V(N));
+    t.W = (double2*)(lds + table_off_W(N));
+    t.Wr = (double2*)(lds + table_off_Wr(N));
+    t.lut = (LutEntry*)(lds + table_off_lut(N));
+    const uint4* g = (const uint4*)gtab;
+    uint4* l = (uint4*)lds;
+    const int iW = (int)(table_off_W(N) / 16), iWr = (int)(table_off_Wr(N) / 16);
+    const int n16 = (int)(table_bytes(N) / 16);
+    for (int i = threadIdx.x; i < n16; i += blockDim.x) {
+        if (i < iW && !needV) continue;
+        if (i >= iW && i < iWr && !needW) continue;
+        l[i] = g[i];
+    }
+    return t;
+}
+
+// One forward step p <- V + r (p - V), each operation rounded on its own.
+__device__ inline void encode_step(double& px, double& py, const double2 v, const double r)
+{
+    const double tx = px - v.x;
+    const double ty = py - v.y;
+    const double ux = r * tx;
+    const double uy = r * ty;
+    px = v.x + ux;
+    py = v.y + uy;
+}
+
+// Sector of a point from the pseudo-angle look-up table.  Exact for every
+// point at least kFastSectorMargin away from the sector lines (the fp32
+// pseudo-angle errs by < 1e-6 there); never leaves [0, N).
+__device__ inline int sector_fast(double qx, double qy, const LutEntry* __restrict__ lut)
+{
+    const float fx = (float)qx;
+    const float fy = (float)qy;
+    const float s = fabsf(fx) + fabsf(fy);
+    const float d = fy * __builtin_amdgcn_rcpf(s);
+    float P = fx >= 0.0f ? d : 2.0f - d;
+    P = fminf(fmaxf(P, -1.0f), 2.99999f);   // NaN (zero or non-finite input) -> -1
+    int idx = (int)((P + 1.0f) * (float)kLutPerUnit);
+    idx = min(idx, kLutBuckets - 1);
+    const LutEntry e = lut[idx];
+    return P >= e.thr ? e.hi : e.lo;
+}
+
+// Exact nearest cell centre, lowest index on exact ties (used when the margin
+// cannot be certified, e.g. touching cells at r = r_N).
+__device__ inline int sector_exact(double qx, double qy, const double2* __restrict__ W, int N)
+{
+    int best = 0;
+    double dx = qx - W[0].x, dy = qy - W[0].y;
+    double bd = dx * dx + dy * dy;
+    for (int c = 1; c < N; ++c) {
+        dx = qx - W[c].x;
+        dy = qy - W[c].y;
+        const double d = dx * dx + dy * dy;
+        if (d < bd) {
+            bd = d;
+            best = c;
+        }
+    }
+    return best;
+}
+
+template <bool EXACT>
+__device__ inline int sector_of(double qx, double qy, const Tables& t, int N)
+{
+    if (EXACT) return sector_exact(qx, qy, t.W, N);
+    return sector_fast(qx, qy, t.lut);
+}
+
+// Inverse map q <- (q - W(c)) / r, as q * (1/r) - W(c)/r with one rounding per
+// coordinate.
+__device__ inline void decode_step(double& qx, double& qy, const double2 wr, const double inv_r)
+{
+    qx = __builtin_fma(qx, inv_r, -wr.x);
+    qy = __builtin_fma(qy, inv_r, -wr.y);
+}
+
+__device__ inline bool anchor_ok(double qx, double qy)
+{
+    const double a = fmax(fabs(qx), fabs(qy));
+    return a <= kAnchorTol && qx == qx && qy == qy;
+}
+
+// Random access to one token (Sec. 2, Table 1): decodes only the span(s) of
+// stream s holding symbols [tk*S, tk*S + S) and packs them into *got (byte k =
+// symbol k).  P0 is the point of the first such span when the caller already
+// loaded it (has_p0).  Returns 1 when a decoded span fails its anchor check.
+template <bool EXACT>
+__device__ inline int lookup_token(const double2* __restrict__ pts, const Tables& t, const CodecArgs& cd,
+                                   int64_t s, int64_t tk, int S, int64_t n_sym, int64_t n_spans,
+                                   bool has_p0, double2 P0, uint64_t* got)
+{
+    const int L = cd.L;
+    const int64_t a = tk * S;
+    const int64_t j0 = a / L, j1 = (a + S - 1) / L;
+    int status = 0;
+    uint64_t g = 0;
+    for (int64_t j = j0; j <= j1; ++j) {
+        const int64_t b = j * L;
+        const int len = (int)min((int64_t)L, n_sym - b);
+        const double2 P = (has_p0 && j == j0) ? P0 : pts[s * n_spans + j];
+        double qx = P.x, qy = P.y;
+        for (int k = len - 1; k >= 0; --k) {
+            const int c = sector_of<EXACT>(qx, qy, t, cd.N);
+            const int64_t off = b + k - a;   // position within the token's S symbols
+            if (off >= 0 && off < S) g |= (uint64_t)c << (8 * off);
+            decode_step(qx, qy, t.Wr[c], cd.inv_r);
+        }
+        if (!anchor_ok(qx, qy)) status = 1;
+    }
+    *got = g;
+    return status;
+}
+
+int64_t blocks_for(int64_t n_tiles)
+{
+    return n_tiles < kMaxBlocks ? (n_tiles > 0 ? n_tiles : 1) : kMaxBlocks;
+}
+
+bool codec_ok(const fkv_codec* c)
+{
+    return c && c->N >= 3 && c->N <= 256 && c->L >= 1 && c->L <= 64 && c->r > 0.0 && c->r < 1.0 &&
+           c->r_max > 0.0 && c->r <= c->r_max * (1.0 + 1e-12);
+}
+
+CodecArgs codec_args(const fkv_codec* c)
+{
+    CodecArgs a;
+    a.N = c->N;
+    a.L = c->L;
+    a.r = c->r;
+    a.inv_r = 1.0 / c->r;
+    return a;
+}
+
+// The look-up path is exact when every valid point keeps a margin of at least
+// kFastSectorMargin from the sector lines: that margin is sin(pi/N) (1 - r/r_N).
+bool needs_exact_sectors(const fkv_codec* c)
+{
+    const double margin = sin(M_PI / (double)c->N) * (1.0 - c->r / c->r_max);
+    return !(margin >= kFastSectorMargin);
+}
+
+}  // namespace
+}  // namespace fkv

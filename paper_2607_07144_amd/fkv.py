@@ -47,6 +47,9 @@ _SIGS = {
     "fkv_cgr_encode_spans": ([_PC, _p, _p, _i64, _i64, _p, _p], ctypes.c_int),
     "fkv_cgr_decode_spans": ([_PC, _p, _p, _i64, _i64, _p, _p, _p, _i32, _p], ctypes.c_int),
     "fkv_span_lookup": ([_PC, _p, _p, _i64, _i64, _i32, _p, _p, _i64, _p, _p, _p, _p], ctypes.c_int),
+    "fkv_rehydrate": ([_PC, _p, _p, _i64, _i64, _i32, _p, _p, _i32, _i32, _i32, _p, _p, _i64, _p, _p, _p, _p],
+                      ctypes.c_int),
+    "fkv_cgr_append": ([_PC, _p, _p, _i64, _i64, _i64, _p, _i64, _p], ctypes.c_int),
     "fkv_status_string": ([ctypes.c_int], ctypes.c_char_p),
     "fkv_version": ([], ctypes.c_char_p),
 }
@@ -222,6 +225,54 @@ def fkv_span_lookup(codec: Codec, points, n_sym: int, S: int, q_stream, q_token,
                                n_sym, S, _ptr(q_stream), _ptr(q_token), nq, _ptr(out), _ptr(q_status),
                                _ptr(n_failed), _stream(stream)), "fkv_span_lookup")
     return out
+
+
+# ------------------------------------------------------------------ rehydrate / append
+
+def fkv_rehydrate(codec: Codec, points, n_sym: int, S: int, books, stream_book, q_stream, q_token, out=None,
+                  q_status=None, n_failed=None, stream=None):
+    """Reconstruction of archived positions: out f16 [n_q][d], the sum of each queried token's S
+    codewords (symbols read back by random access), correctly rounded to binary16."""
+    torch = _torch()
+    _need(points, torch.float64, "points")
+    _need(books, torch.float16, "books")
+    _need(stream_book, torch.int32, "stream_book")
+    _need(q_stream, torch.int32, "q_stream")
+    _need(q_token, torch.int32, "q_token")
+    nb, S2, K, d = books.shape
+    if S2 != S:
+        raise ValueError("books has %d stages, S = %d" % (S2, S))
+    nq = q_stream.numel()
+    if q_token.numel() != nq:
+        raise ValueError("q_stream and q_token differ in length")
+    if out is None:
+        out = torch.empty((nq, d), dtype=torch.float16, device=points.device)
+    _need(out, torch.float16, "out")
+    if q_status is not None:
+        _need(q_status, torch.uint8, "q_status")
+    if n_failed is not None:
+        _need(n_failed, torch.int32, "n_failed")
+    ns = points.shape[0]
+    if stream_book.numel() != ns:
+        raise ValueError("stream_book must have one entry per stream")
+    _check(lib.fkv_rehydrate(ctypes.byref(codec.c), _ptr(codec.table(points.device)), _ptr(points), ns, n_sym,
+                             S, _ptr(books), _ptr(stream_book), nb, K, d, _ptr(q_stream), _ptr(q_token), nq,
+                             _ptr(out), _ptr(q_status), _ptr(n_failed), _stream(stream)), "fkv_rehydrate")
+    return out
+
+
+def fkv_cgr_append(codec: Codec, points, n_old: int, sym_new, stream=None):
+    """Append sym_new u8 [n_streams][m] to every stream of n_old symbols; points f64
+    [n_streams][cap_spans][2] is updated in place."""
+    torch = _torch()
+    _need(points, torch.float64, "points")
+    _need(sym_new, torch.uint8, "sym_new")
+    ns, cap = points.shape[0], points.shape[1]
+    if sym_new.dim() != 2 or sym_new.shape[0] != ns:
+        raise ValueError("sym_new must be [n_streams][m]")
+    _check(lib.fkv_cgr_append(ctypes.byref(codec.c), _ptr(codec.table(points.device)), _ptr(points), cap, ns,
+                              n_old, _ptr(sym_new), sym_new.shape[1], _stream(stream)), "fkv_cgr_append")
+    return points
 
 
 def fkv_version() -> str:

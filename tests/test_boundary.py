@@ -158,3 +158,39 @@ def test_invalid_arguments_are_rejected_on_the_host(F):
     assert rvq(D(4, 100, 4, 68, 64, 2, 256, 4), res=P(0x10004)) == E
     assert rvq(D(0, 100, 4, 68, 64, 2, 256, 4), x=None, b=None, sb=None, sym=None) == 0
     assert rvq(D(4, 100, 10, 10, 64, 2, 256, 4), x=None, b=None, sb=None, sym=None) == 0
+
+
+def test_invalid_arguments_rehydrate_and_append(F):
+    lib = F.lib
+    E = F.FKV_ERR_INVALID_ARG
+    c = F.fkv_codec()
+    assert lib.fkv_codec_init(16, 0.98, 0, ctypes.byref(c)) == 0
+    P = ctypes.c_void_p
+    g, odd = P(0x10000), P(0x10008)
+
+    def rh(ns=1, n_sym=10, S=2, books=g, sb=g, nb=1, K=16, d=64, qs=g, qt=g, nq=5, out=g, codec=c):
+        return lib.fkv_rehydrate(ctypes.byref(codec), g, g, ns, n_sym, S, books, sb, nb, K, d, qs, qt, nq, out,
+                                 None, None, None)
+
+    assert rh(S=3) == E                 # n_sym not a multiple of S
+    assert rh(S=9, n_sym=18) == E       # S > 8
+    assert rh(K=0) == E and rh(K=257) == E
+    assert rh(d=12) == E and rh(d=264) == E and rh(d=0) == E
+    assert rh(nb=0) == E
+    assert rh(books=None) == E and rh(books=odd) == E
+    assert rh(out=None) == E and rh(out=odd) == E
+    assert rh(sb=None) == E
+    assert rh(qs=None) == E
+    assert rh(codec=F.fkv_codec(16, 0, 0.1, 0.2)) == E
+    assert rh(nq=0, books=None, out=None, qs=None, qt=None) == 0     # no queries: nothing enqueued
+
+    def ap(cap=2, ns=1, n_old=10, sym=g, m=3, pts=g, codec=c):
+        return lib.fkv_cgr_append(ctypes.byref(codec), g, pts, cap, ns, n_old, sym, m, None)
+
+    assert c.L == 16
+    assert ap(cap=0) == E               # ceil(13 / 16) = 1 span needed
+    assert ap(n_old=30, cap=2, m=3) == E   # 33 symbols need 3 spans
+    assert ap(m=-1) == E and ap(n_old=-1) == E and ap(ns=-1) == E
+    assert ap(sym=None) == E and ap(pts=None) == E and ap(pts=odd) == E
+    assert ap(codec=F.fkv_codec(16, 0, 0.1, 0.2)) == E
+    assert ap(m=0, sym=None, pts=None) == 0 and ap(ns=0, sym=None, pts=None) == 0
