@@ -139,6 +139,71 @@ def algorithmic(cfg, groups):
     return a
 
 
+def time_graph(fn, reps: int, replays: int, stream):
+    """Average duration of one fn() call: a graph of `reps` back-to-back calls, replayed and
+    bracketed by events on the stream the replays run on."""
+    import torch
+
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=stream):
+        for _ in range(reps):
+            fn()
+    g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(replays):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / 1e3 / (reps * replays)
+
+
+def next_rows(fkv, cfg, groups, side, replays: int):
+    """Measurements of the rows beyond the step: rehydration of the step's lookup queries, and one
+    decoding step's archive update (the position leaving the recent window is assigned on every
+    stream and its symbols appended)."""
+    import torch
+
+    res = {"rehydrate": {"queries": 0, "bytes": 0, "s": 0.0}, "evict_append": {"s": 0.0, "bytes": 0}}
+    with torch.cuda.stream(side):
+        for gr in groups:
+            g = gr["g"]
+            nq = gr["qs"].numel()
+            out = torch.empty((nq, cfg.d), dtype=torch.float16, device="cuda")
+            t = time_graph(lambda: fkv.fkv_rehydrate(gr["codec"], gr["pts"], gr["n_sym"], g.S, gr["books"],
+                                                     gr["sb"], gr["qs"], gr["qt"], out=out), 10, replays, side)
+            L = gr["codec"].L
+            qt = gr["qt_h"].astype(np.int64) * g.S
+            spans = int(((qt + g.S - 1) // L - qt // L + 1).sum())
+            res["rehydrate"]["queries"] += nq
+            res["rehydrate"]["bytes"] += nq * (8 + g.S * cfg.d * 2 + cfg.d * 2) + 16 * spans
+            res["rehydrate"]["s"] += t
+            # one eviction: token t_end - 1 of every stream, appended after the archived symbols
+            ns = gr["ns"]
+            n_old = gr["n_sym"] - g.S
+            pts = gr["pts"].clone()
+            sym1 = torch.empty((ns, g.S), dtype=torch.uint8, device="cuda")
+
+            def step():
+                fkv.fkv_rvq_assign(gr["x"], gr["books"], gr["sb"], cfg.t_end - 1, cfg.t_end, symbols=sym1)
+                fkv.fkv_cgr_append(gr["codec"], pts, n_old, sym1)
+
+            res["evict_append"]["s"] += time_graph(step, 10, replays, side)
+            res["evict_append"]["bytes"] += ns * (cfg.d * 2 + g.S) + gr["books"].numel() * 2 + ns * 32
+    rh, ev = res["rehydrate"], res["evict_append"]
+    ach = rh["bytes"] / rh["s"] / 1e9
+    return {
+        "rehydrate": {"queries": rh["queries"], "avg_launch_us": round(rh["s"] / len(groups) * 1e6, 2),
+                      "queries_per_s": round(rh["queries"] / rh["s"], 1),
+                      "roofline": {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                                   "frac": round(ach / PEAK_HBM_GBS, 4)}},
+        "evict_append": {"us_per_decoding_step": round(ev["s"] * 1e6, 2),
+                         "positions_per_s": round(1.0 / ev["s"], 1),
+                         "streams": sum(gr["ns"] for gr in groups)},
+    }
+
+
 def cpu_baseline(cfg, groups, max_streams: int):
     """The CPU oracle on (a sample of) the same step, all host cores, extrapolated per token."""
     import oracle
@@ -242,6 +307,7 @@ def main():
         torch.cuda.synchronize()
         phase_ms[n] = e0.elapsed_time(e1) / (reps * max(1, args.steps // 4))
 
+    extra = next_rows(fkv, cfg, groups, side, max(1, args.steps // 4))
     alg = algorithmic(cfg, groups)
     tokens = cfg.batch * cfg.T_arch
     launches = len(groups)
@@ -288,6 +354,7 @@ def main():
         "lookups_per_s": round(alg["lookups"] / (phase_ms["span_lookup"] / 1e3), 1),
         "roofline": roof,
         "rooflines": rooflines,
+        "next_rows": extra,
         "cpu_baseline": None,
     }
     if not args.no_cpu_baseline:

@@ -193,6 +193,29 @@ int fkv_rehydrate(const fkv_codec* c, const void* dev_table, const double* point
 int fkv_cgr_append(const fkv_codec* c, const void* dev_table, double* points, int64_t cap_spans,
                    int64_t n_streams, int64_t n_old, const uint8_t* sym_new, int64_t m, void* stream);
 
+/* ---- in-archive retrieval (Sec. 5) ---------------------------------------
+ * Per-position index: traj[s][k] (device f64 pairs [n_streams][n_sym][2],
+ * 16-byte aligned) is the point of the walk over the W symbols ending at
+ * position k of stream s (positions max(0, k-W+1)..k), started at the origin
+ * (1 <= W <= 64).  symbols: device u8 [n_streams][n_sym], 4-byte aligned. */
+int fkv_trajectory(const fkv_codec* c, const void* dev_table, const uint8_t* symbols, int64_t n_streams,
+                   int64_t n_sym, int32_t W, double* traj, void* stream);
+
+/* Suffix search on the index: the query (device u8 [ell], 1 <= ell <= L and
+ * ell <= the index's W) is encoded from the origin to q; every position k >=
+ * ell-1 whose point p has |p - q|^2 <= (2 r^ell)^2 is a candidate (a position
+ * whose last ell symbols equal the query lies within r^ell, so none is
+ * missed); with verify = 1 a candidate is kept only when decoding ell symbols
+ * backward from p reproduces the query, with verify = 0 every candidate is a
+ * hit.  Hits are written as (stream, position) u32 pairs to hits
+ * [max_hits][2] (8-byte aligned; order unspecified, at most max_hits);
+ * *n_hits (device u32, required) += the number of hits, *n_candidates
+ * (nullable) += the number of candidates.  A query symbol >= N matches
+ * nothing. */
+int fkv_suffix_search(const fkv_codec* c, const void* dev_table, const double* traj, int64_t n_streams,
+                      int64_t n_sym, const uint8_t* query, int32_t ell, int32_t verify, uint32_t* hits,
+                      int64_t max_hits, uint32_t* n_hits, uint32_t* n_candidates, void* stream);
+
 /* Static description of a status code. */
 const char* fkv_status_string(int status);
 

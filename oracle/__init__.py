@@ -69,6 +69,11 @@ def _load():
     lib.fkvo_rehydrate.restype = c_i64
     lib.fkvo_append.argtypes = [c_i32, c_dbl, c_i32, c_p, c_p, c_i64, c_i64, c_i64, c_p, c_i64, c_i32]
     lib.fkvo_append.restype = None
+    lib.fkvo_trajectory.argtypes = [c_i32, c_dbl, c_p, c_p, c_i64, c_i64, c_i32, c_p, c_i32]
+    lib.fkvo_trajectory.restype = None
+    lib.fkvo_suffix_search.argtypes = [c_i32, c_dbl, c_p, c_p, c_p, c_i64, c_i64, c_p, c_i32, c_i32, c_p,
+                                       c_i64, c_p]
+    lib.fkvo_suffix_search.restype = c_i64
     _lib = lib
     return lib
 
@@ -244,3 +249,36 @@ def append(codec: Codec, points: np.ndarray, n_old: int, sym_new: np.ndarray,
     _load().fkvo_append(codec.N, codec.r, codec.L, _ptr(codec.V), _ptr(pts), cap, ns, n_old, _ptr(sym),
                         m, threads or default_threads())
     return pts
+
+
+def trajectory(codec: Codec, symbols: np.ndarray, W: int, threads: int | None = None) -> np.ndarray:
+    """Per-position index (Sec. 5): traj f64 [n_streams][n_sym][2], the point of the walk over the
+    W symbols ending at each position, from the origin."""
+    sym = np.ascontiguousarray(symbols, dtype=np.uint8)
+    if sym.ndim == 1:
+        sym = sym[None, :]
+    ns, n = sym.shape
+    if n and int(sym.max()) >= codec.N:
+        raise ValueError("symbol out of alphabet")
+    if not 1 <= W <= 64:
+        raise ValueError("W must be in 1..64")
+    out = np.zeros((ns, n, 2), np.float64)
+    _load().fkvo_trajectory(codec.N, codec.r, _ptr(codec.V), _ptr(sym), ns, n, W, _ptr(out),
+                            threads or default_threads())
+    return out
+
+
+def suffix_search(codec: Codec, traj: np.ndarray, query: np.ndarray, verify: bool = True,
+                  max_hits: int = 1 << 20):
+    """Suffix search on the index (Sec. 5) -> (hits u32 [n][2] as (stream, position), n_hits,
+    n_candidates)."""
+    tr = np.ascontiguousarray(traj, dtype=np.float64)
+    q = np.ascontiguousarray(query, dtype=np.uint8)
+    if not 1 <= q.size <= codec.L:
+        raise ValueError("query length must be in 1..L")
+    ns, n = tr.shape[0], tr.shape[1]
+    hits = np.zeros((max_hits, 2), np.uint32)
+    nc = np.zeros(1, np.int64)
+    nh = _load().fkvo_suffix_search(codec.N, codec.r, _ptr(codec.V), _ptr(codec.W), _ptr(tr), ns, n, _ptr(q),
+                                    q.size, 1 if verify else 0, _ptr(hits), max_hits, _ptr(nc))
+    return hits[:min(nh, max_hits)], int(nh), int(nc[0])

@@ -436,3 +436,78 @@ void fkvo_append(int32_t N, double r, int32_t L, const double* V, double* points
         }
     }
 }
+
+/* ------------------------------------------------------------- retrieval -- */
+
+/*
+ * Sec. 5: the archive is searchable in place.  Per-position index: for every
+ * symbol position k of a stream, traj[k] is the point of the walk over the W
+ * symbols ending at k (positions max(0, k-W+1)..k), started at the origin.
+ * (The contraction makes older symbols' weight r^age; windows of W symbols
+ * keep every position independent, the reading taken for a parallel layout.)
+ */
+void fkvo_trajectory(int32_t N, double r, const double* V, const uint8_t* symbols,
+                     int64_t n_streams, int64_t n_sym, int32_t W, double* traj, int32_t threads)
+{
+    (void)N;
+#pragma omp parallel for schedule(static) num_threads(threads)
+    for (int64_t s = 0; s < n_streams; ++s)
+        for (int64_t k = 0; k < n_sym; ++k) {
+            int64_t a = k - W + 1 > 0 ? k - W + 1 : 0;
+            encode_one(r, V, symbols + s * n_sym + a, k - a + 1, &traj[(s * n_sym + k) * 2],
+                       &traj[(s * n_sym + k) * 2 + 1]);
+        }
+}
+
+/*
+ * Sec. 5 suffix search: the query (ell symbols, ell <= W and ell <= L) is
+ * encoded from the origin to q; every indexed position k >= ell - 1 (one with
+ * ell symbols of history) whose point p has |p - q|^2 <= (2 r^ell)^2 is a
+ * candidate (two walks sharing their last ell symbols end within r^ell of each
+ * other, so no true match is missed while r^ell stays far above the rounding
+ * of the points, which ell <= L guarantees).  With verify, a candidate is kept only
+ * when decoding ell symbols backward from p reproduces the query.  Hits are
+ * written as (stream, position) pairs in stream-major, position order (at most
+ * max_hits); returns the number of hits, *n_candidates gets the candidates.
+ * The threshold is 2 * r^ell with r^ell formed by ell successive products.
+ */
+int64_t fkvo_suffix_search(int32_t N, double r, const double* V, const double* W_,
+                           const double* traj, int64_t n_streams, int64_t n_sym,
+                           const uint8_t* query, int32_t ell, int32_t verify,
+                           uint32_t* hits, int64_t max_hits, int64_t* n_candidates)
+{
+    double qx, qy;
+    encode_one(r, V, query, ell, &qx, &qy);
+    double rl = 1.0;
+    for (int32_t k = 0; k < ell; ++k) rl = rl * r;
+    double thr = 2.0 * rl;
+    double thr2 = thr * thr;
+    int64_t n_hit = 0, n_cand = 0;
+    for (int64_t s = 0; s < n_streams; ++s)
+        for (int64_t k = ell - 1; k < n_sym; ++k) {
+            const double* p = &traj[(s * n_sym + k) * 2];
+            double dx = p[0] - qx, dy = p[1] - qy;
+            double d2 = dx * dx + dy * dy;
+            if (!(d2 <= thr2)) continue;
+            n_cand += 1;
+            if (verify) {
+                /* the cell of the point is the last symbol; invert and repeat */
+                double x = p[0], y = p[1];
+                int ok = 1;
+                for (int32_t j = ell - 1; j >= 0 && ok; --j) {
+                    int32_t c = fkvo_cell(N, W_, x, y);
+                    if (c != query[j]) ok = 0;
+                    x = (x - W_[2 * c]) / r;
+                    y = (y - W_[2 * c + 1]) / r;
+                }
+                if (!ok) continue;
+            }
+            if (n_hit < max_hits) {
+                hits[n_hit * 2] = (uint32_t)s;
+                hits[n_hit * 2 + 1] = (uint32_t)k;
+            }
+            n_hit += 1;
+        }
+    if (n_candidates) *n_candidates = n_cand;
+    return n_hit;
+}

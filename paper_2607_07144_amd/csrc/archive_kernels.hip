@@ -142,6 +142,116 @@ __global__ __launch_bounds__(kBlock) void append_kernel(double2* __restrict__ pt
     }
 }
 
+// --------------------------------------------------------------- retrieval --
+// Sec. 5: the per-position index holds, for every symbol position k, the
+// point of the walk over the W symbols ending at k, from the origin (one lane
+// per position: W forward steps over a symbol tile staged in LDS).  A suffix
+// query of ell symbols is encoded from the origin to q; every indexed position
+// with ell symbols of history whose point lies within 2 r^ell of q is a
+// candidate, kept when decoding ell symbols backward from it reproduces the
+// query.  The scan streams the index once (16 bytes per position).
+
+__global__ __launch_bounds__(kBlock) void trajectory_kernel(const uint8_t* __restrict__ sym,
+                                                             double2* __restrict__ traj,
+                                                             const uint8_t* __restrict__ gtab, CodecArgs cd,
+                                                             int64_t n_sym, int W, int64_t tiles_per_stream,
+                                                             int64_t n_tiles)
+{
+    extern __shared__ __align__(16) uint8_t lds[];
+    const int N = cd.N;
+    double2* V = (double2*)lds;
+    uint8_t* tile = lds + 256 * sizeof(double2);
+    V[threadIdx.x] = (int)threadIdx.x < N ? ((const double2*)(gtab + table_off_V(N)))[threadIdx.x]
+                                          : make_double2(NAN, NAN);
+    for (int64_t tl = blockIdx.x; tl < n_tiles; tl += gridDim.x) {
+        const int64_t s = tl / tiles_per_stream;
+        const int64_t k0 = (tl - s * tiles_per_stream) * kBlock;
+        const int64_t a0 = max((int64_t)0, k0 - W + 1);
+        const int64_t k1 = min(n_sym, k0 + kBlock);
+        const int64_t g0 = s * n_sym + a0, g1 = s * n_sym + k1;
+        __syncthreads();   // previous tile consumed
+        bytes_to_lds(sym, g0, g1, tile);
+        __syncthreads();
+        const int64_t k = k0 + threadIdx.x;
+        if (k < k1) {
+            const int64_t a = max((int64_t)0, k - W + 1);
+            const uint8_t* my = tile + (g0 & 3) + (a - a0);
+            double px = 0.0, py = 0.0;
+            for (int64_t j = 0; j <= k - a; ++j) encode_step(px, py, V[my[j]], cd.r);
+            traj[s * n_sym + k] = make_double2(px, py);
+        }
+    }
+}
+
+template <bool EXACT, bool VERIFY>
+__global__ __launch_bounds__(kBlock) void suffix_search_kernel(
+    const double2* __restrict__ traj, const uint8_t* __restrict__ query, const uint8_t* __restrict__ gtab,
+    CodecArgs cd, int64_t n_streams, int64_t n_sym, int ell, uint32_t* __restrict__ hits, int64_t max_hits,
+    uint32_t* __restrict__ n_hits, uint32_t* __restrict__ n_cand)
+{
+    extern __shared__ __align__(16) uint8_t lds[];
+    const int N = cd.N;
+    Tables t = stage_tables(gtab, N, lds, true, EXACT);
+    uint8_t* qs = lds + table_bytes(N);
+    if ((int)threadIdx.x < ell) qs[threadIdx.x] = query[threadIdx.x];
+    __syncthreads();
+    // the query's point from the origin and the threshold, as in the index; a
+    // query symbol outside the alphabet matches nothing
+    bool qok = true;
+    for (int j = 0; j < ell; ++j) qok = qok && qs[j] < N;
+    double qx = 0.0, qy = 0.0;
+    for (int j = 0; j < ell; ++j) encode_step(qx, qy, t.V[qok ? qs[j] : 0], cd.r);
+    double rl = 1.0;
+    for (int j = 0; j < ell; ++j) rl = rl * cd.r;
+    const double thr = 2.0 * rl;
+    const double thr2 = thr * thr;
+    const int64_t total = n_streams * n_sym;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    const int64_t n_iter = (total + stride - 1) / stride;   // same trip count for every lane
+    const int lane = threadIdx.x & 63;
+    for (int64_t it = 0; it < n_iter; ++it) {
+        const int64_t i = it * stride + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+        bool cand = false, hit = false;
+        int64_t s = 0, k = 0;
+        if (i < total) {
+            s = i / n_sym;
+            k = i - s * n_sym;
+            if (qok && k >= ell - 1) {
+                const double2 p = traj[i];
+                const double dx = p.x - qx, dy = p.y - qy;
+                const double d2 = dx * dx + dy * dy;
+                cand = d2 <= thr2;
+                hit = cand;
+                if (VERIFY && cand) {
+                    double x = p.x, y = p.y;
+                    for (int j = ell - 1; j >= 0; --j) {
+                        const int c = sector_of<EXACT>(x, y, t, N);
+                        if (c != qs[j]) {
+                            hit = false;
+                            break;
+                        }
+                        decode_step(x, y, t.Wr[c], cd.inv_r);
+                    }
+                }
+            }
+        }
+        const unsigned long long mc = __ballot(cand), mh = __ballot(hit);
+        if (n_cand && mc && lane == 0) atomicAdd(n_cand, (uint32_t)__popcll(mc));
+        if (mh) {
+            uint32_t base = 0;
+            if (lane == 0) base = atomicAdd(n_hits, (uint32_t)__popcll(mh));
+            base = __shfl(base, 0);
+            if (hit) {
+                const int64_t slot = (int64_t)base + __popcll(mh & ((1ull << lane) - 1));
+                if (slot < max_hits) {
+                    hits[2 * slot] = (uint32_t)s;
+                    hits[2 * slot + 1] = (uint32_t)k;
+                }
+            }
+        }
+    }
+}
+
 }  // namespace
 }  // namespace fkv
 
@@ -194,5 +304,55 @@ extern "C" int fkv_cgr_append(const fkv_codec* c, const void* dev_table, double*
     hipLaunchKernelGGL(append_kernel, dim3((unsigned)nb), dim3(kBlock), 0, (hipStream_t)stream,
                        (double2*)points, sym_new, (const uint8_t*)dev_table, codec_args(c), cap_spans, n_streams,
                        n_old, m);
+    return launch_status();
+}
+
+extern "C" int fkv_trajectory(const fkv_codec* c, const void* dev_table, const uint8_t* symbols,
+                              int64_t n_streams, int64_t n_sym, int32_t W, double* traj, void* stream)
+{
+    if (!codec_ok(c) || !dev_table || n_streams < 0 || n_sym < 0 || W < 1 || W > 64) return FKV_ERR_INVALID_ARG;
+    if (n_streams == 0 || n_sym == 0) return FKV_OK;
+    if (!symbols || !traj || !aligned(symbols, 4) || !aligned(traj, 16) || !aligned(dev_table, 16))
+        return FKV_ERR_INVALID_ARG;
+    const int64_t tps = (n_sym + kBlock - 1) / kBlock;
+    const int64_t n_tiles = tps * n_streams;
+    const size_t shm = 256 * 16 + (size_t)kBlock + 64 + 16;
+    hipLaunchKernelGGL(trajectory_kernel, dim3((unsigned)blocks_for(n_tiles)), dim3(kBlock), shm,
+                       (hipStream_t)stream, symbols, (double2*)traj, (const uint8_t*)dev_table, codec_args(c), n_sym,
+                       W, tps, n_tiles);
+    return launch_status();
+}
+
+extern "C" int fkv_suffix_search(const fkv_codec* c, const void* dev_table, const double* traj, int64_t n_streams,
+                                 int64_t n_sym, const uint8_t* query, int32_t ell, int32_t verify, uint32_t* hits,
+                                 int64_t max_hits, uint32_t* n_hits, uint32_t* n_candidates, void* stream)
+{
+    if (!codec_ok(c) || !dev_table || n_streams < 0 || n_sym < 0 || max_hits < 0) return FKV_ERR_INVALID_ARG;
+    if (ell < 1 || ell > c->L || (verify != 0 && verify != 1) || !query || !n_hits) return FKV_ERR_INVALID_ARG;
+    if (max_hits > 0 && (!hits || !aligned(hits, 8))) return FKV_ERR_INVALID_ARG;
+    if (!aligned(n_hits, 4) || (n_candidates && !aligned(n_candidates, 4)) || !aligned(dev_table, 16))
+        return FKV_ERR_INVALID_ARG;
+    if (n_streams == 0 || n_sym == 0) return FKV_OK;
+    if (!traj || !aligned(traj, 16)) return FKV_ERR_INVALID_ARG;
+    const size_t shm = table_bytes(c->N) + 64;
+    const int64_t nb = blocks_for((n_streams * n_sym + kBlock - 1) / kBlock);
+    const dim3 grid((unsigned)nb), block(kBlock);
+    const hipStream_t st = (hipStream_t)stream;
+    const double2* T = (const double2*)traj;
+    const uint8_t* tb = (const uint8_t*)dev_table;
+    const CodecArgs a = codec_args(c);
+    const bool exact = needs_exact_sectors(c);
+    if (exact && verify)
+        hipLaunchKernelGGL((suffix_search_kernel<true, true>), grid, block, shm, st, T, query, tb, a, n_streams,
+                           n_sym, ell, hits, max_hits, n_hits, n_candidates);
+    else if (exact)
+        hipLaunchKernelGGL((suffix_search_kernel<true, false>), grid, block, shm, st, T, query, tb, a, n_streams,
+                           n_sym, ell, hits, max_hits, n_hits, n_candidates);
+    else if (verify)
+        hipLaunchKernelGGL((suffix_search_kernel<false, true>), grid, block, shm, st, T, query, tb, a, n_streams,
+                           n_sym, ell, hits, max_hits, n_hits, n_candidates);
+    else
+        hipLaunchKernelGGL((suffix_search_kernel<false, false>), grid, block, shm, st, T, query, tb, a, n_streams,
+                           n_sym, ell, hits, max_hits, n_hits, n_candidates);
     return launch_status();
 }

@@ -50,6 +50,8 @@ _SIGS = {
     "fkv_rehydrate": ([_PC, _p, _p, _i64, _i64, _i32, _p, _p, _i32, _i32, _i32, _p, _p, _i64, _p, _p, _p, _p],
                       ctypes.c_int),
     "fkv_cgr_append": ([_PC, _p, _p, _i64, _i64, _i64, _p, _i64, _p], ctypes.c_int),
+    "fkv_trajectory": ([_PC, _p, _p, _i64, _i64, _i32, _p, _p], ctypes.c_int),
+    "fkv_suffix_search": ([_PC, _p, _p, _i64, _i64, _p, _i32, _i32, _p, _i64, _p, _p, _p], ctypes.c_int),
     "fkv_status_string": ([ctypes.c_int], ctypes.c_char_p),
     "fkv_version": ([], ctypes.c_char_p),
 }
@@ -273,6 +275,43 @@ def fkv_cgr_append(codec: Codec, points, n_old: int, sym_new, stream=None):
     _check(lib.fkv_cgr_append(ctypes.byref(codec.c), _ptr(codec.table(points.device)), _ptr(points), cap, ns,
                               n_old, _ptr(sym_new), sym_new.shape[1], _stream(stream)), "fkv_cgr_append")
     return points
+
+
+# ------------------------------------------------------------------ retrieval
+
+def fkv_trajectory(codec: Codec, symbols, W: int = 0, traj=None, stream=None):
+    """Per-position index: traj f64 [n_streams][n_sym][2] (W = 0 selects W = L)."""
+    torch = _torch()
+    _need(symbols, torch.uint8, "symbols")
+    ns, n = symbols.shape
+    W = W or codec.L
+    if traj is None:
+        traj = torch.empty((ns, n, 2), dtype=torch.float64, device=symbols.device)
+    _need(traj, torch.float64, "traj")
+    _check(lib.fkv_trajectory(ctypes.byref(codec.c), _ptr(codec.table(symbols.device)), _ptr(symbols), ns, n, W,
+                              _ptr(traj), _stream(stream)), "fkv_trajectory")
+    return traj
+
+
+def fkv_suffix_search(codec: Codec, traj, query, verify: bool = True, max_hits: int = 1 << 20, hits=None,
+                      n_hits=None, n_candidates=None, stream=None):
+    """Suffix search: returns (hits u32-as-int32 [max_hits][2], n_hits int32 [1], n_candidates int32 [1]);
+    the first min(n_hits, max_hits) rows of hits are (stream, position) pairs in no particular order."""
+    torch = _torch()
+    _need(traj, torch.float64, "traj")
+    _need(query, torch.uint8, "query")
+    ns, n = traj.shape[0], traj.shape[1]
+    if hits is None:
+        hits = torch.empty((max(max_hits, 1), 2), dtype=torch.int32, device=traj.device)
+    _need(hits, torch.int32, "hits")
+    if n_hits is None:
+        n_hits = torch.zeros(1, dtype=torch.int32, device=traj.device)
+    if n_candidates is None:
+        n_candidates = torch.zeros(1, dtype=torch.int32, device=traj.device)
+    _check(lib.fkv_suffix_search(ctypes.byref(codec.c), _ptr(codec.table(traj.device)), _ptr(traj), ns, n,
+                                 _ptr(query), query.numel(), 1 if verify else 0, _ptr(hits), max_hits,
+                                 _ptr(n_hits), _ptr(n_candidates), _stream(stream)), "fkv_suffix_search")
+    return hits, n_hits, n_candidates
 
 
 def fkv_version() -> str:
