@@ -204,6 +204,60 @@ def next_rows(fkv, cfg, groups, side, replays: int):
     }
 
 
+def read_stress(fkv, side, replays: int):
+    """Read side at HBM scale: the 144-stream x 131,072-token archive (2 symbols per token, N = 256).
+    Bulk decode rotates over 4 copies of the points so that consecutive launches do not hit the
+    memory-side cache; 2^20 random lookups; the per-position retrieval index (build and one suffix
+    scan of 16 bytes per position)."""
+    import torch
+    from paper_2607_07144_amd import workloads
+
+    c = workloads.READ_STRESS
+    sym_h, qs_h, qt_h = workloads.read_stress_inputs()
+    codec = fkv.Codec(c["N"])
+    ns, n_sym = sym_h.shape
+    sym = torch.from_numpy(sym_h).cuda()
+    pts = fkv.fkv_cgr_encode_spans(codec, sym)
+    copies = [pts] + [pts.clone() for _ in range(3)]
+    dec = torch.empty_like(sym)
+    qs, qt = torch.from_numpy(qs_h.astype(np.int32)).cuda(), torch.from_numpy(qt_h.astype(np.int32)).cuda()
+    out = torch.empty((qs.numel(), c["S"]), dtype=torch.uint8, device="cuda")
+    traj = torch.empty((ns, n_sym, 2), dtype=torch.float64, device="cuda")
+    query = sym[5, 1000:1003].contiguous()
+    hits = torch.empty((1 << 16, 2), dtype=torch.int32, device="cuda")
+    nh = torch.zeros(1, dtype=torch.int32, device="cuda")
+    rot = [0]
+
+    def decode():
+        fkv.fkv_cgr_decode_spans(codec, copies[rot[0] % 4], n_sym, symbols=dec)
+        rot[0] += 1
+
+    with torch.cuda.stream(side):
+        t_dec = time_graph(decode, 8, replays, side)
+        t_lk = time_graph(lambda: fkv.fkv_span_lookup(codec, pts, n_sym, c["S"], qs, qt, out=out), 4, replays, side)
+        t_tr = time_graph(lambda: fkv.fkv_trajectory(codec, sym, traj=traj), 2, replays, side)
+        t_sc = time_graph(lambda: fkv.fkv_suffix_search(codec, traj, query, max_hits=1 << 16, hits=hits,
+                                                        n_hits=nh), 4, replays, side)
+    n_pos = ns * n_sym
+    dec_bytes = n_pos + pts.numel() * 8
+    L = codec.L
+    a = qt_h.astype(np.int64) * c["S"]
+    lk_bytes = int(qs_h.size * (8 + c["S"]) + 16 * ((a + c["S"] - 1) // L - a // L + 1).sum())
+    hbm = lambda b, t: {"bound": "hbm", "achieved": round(b / t / 1e9, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                        "frac": round(b / t / 1e9 / PEAK_HBM_GBS, 4)}
+    return {
+        "archive": "%d streams x %d symbols, N=%d, L=%d" % (ns, n_sym, c["N"], L),
+        "bulk_decode": {"avg_launch_us": round(t_dec * 1e6, 2), "symbols_per_s": round(n_pos / t_dec, 1),
+                        "roofline": hbm(dec_bytes, t_dec), "rotation": 4},
+        "lookup": {"queries": int(qs_h.size), "avg_launch_us": round(t_lk * 1e6, 2),
+                   "lookups_per_s": round(qs_h.size / t_lk, 1), "roofline": hbm(lk_bytes, t_lk)},
+        "index_build": {"avg_launch_us": round(t_tr * 1e6, 2), "positions_per_s": round(n_pos / t_tr, 1),
+                        "roofline": hbm(n_pos * 17, t_tr)},
+        "suffix_scan": {"avg_launch_us": round(t_sc * 1e6, 2), "positions_per_s": round(n_pos / t_sc, 1),
+                        "query_len": 3, "roofline": hbm(n_pos * 16, t_sc)},
+    }
+
+
 def cpu_baseline(cfg, groups, max_streams: int):
     """The CPU oracle on (a sample of) the same step, all host cores, extrapolated per token."""
     import oracle
@@ -244,6 +298,8 @@ def main():
     ap.add_argument("--cpu-streams", type=int, default=288,
                     help="streams per group the CPU oracle baseline runs on")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-read-stress", action="store_true",
+                    help="skip the read-side measurements on the 144 x 131,072-token archive")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="also run one streaming elementwise kernel (torch.neg) that reads and writes "
                          "this many MiB before the step: a kernel of known traffic for scaling HBM "
@@ -308,6 +364,8 @@ def main():
         phase_ms[n] = e0.elapsed_time(e1) / (reps * max(1, args.steps // 4))
 
     extra = next_rows(fkv, cfg, groups, side, max(1, args.steps // 4))
+    if not args.no_read_stress:
+        extra["read_stress"] = read_stress(fkv, side, max(1, args.steps // 4))
     alg = algorithmic(cfg, groups)
     tokens = cfg.batch * cfg.T_arch
     launches = len(groups)

@@ -216,6 +216,27 @@ int fkv_suffix_search(const fkv_codec* c, const void* dev_table, const double* t
                       int64_t n_sym, const uint8_t* query, int32_t ell, int32_t verify, uint32_t* hits,
                       int64_t max_hits, uint32_t* n_hits, uint32_t* n_candidates, void* stream);
 
+/* ---- k-means codebook update (Sec. 3 "Setup": codebooks are trained by
+ * k-means) -------------------------------------------------------------------
+ * One Lloyd update of residual stage `stage` (0 <= stage < S) of the books,
+ * after an assignment by fkv_rvq_assign (symbols [n_streams][(t_end-t_begin)*S]).
+ * fkv_kmeans_accumulate adds, for every archived token of every stream whose
+ * book id is valid and whose symbols of stages 0..stage are < K, the stage
+ * input r = x_t - sum_{st<stage} C[b][st][i_st] to
+ *     sums[b][i_stage][0..d)   (device int64, units of 2^-24: exact integers)
+ * and 1 to counts[b][i_stage] (device u32).  The caller zeroes both; desc is
+ * read as for fkv_rvq_assign, except that d only has to be a multiple of 8
+ * (8..256).  x, books: 16-byte aligned; sums 8-byte aligned.
+ * fkv_kmeans_finalize replaces, for every cluster with count > 0, row
+ * books[b][stage][j] by the mean sums / count * 2^-24 (fp64) rounded once to
+ * binary16 (round to nearest, ties to even); an empty cluster keeps its
+ * centroid. */
+int fkv_kmeans_accumulate(const fkv_rvq_desc* desc, const uint16_t* x_f16, const uint16_t* books_f16,
+                          const int32_t* stream_book, const uint8_t* symbols, int32_t stage, int64_t* sums,
+                          uint32_t* counts, void* stream);
+int fkv_kmeans_finalize(int32_t n_books, int32_t S, int32_t K, int32_t d, int32_t stage, const int64_t* sums,
+                        const uint32_t* counts, uint16_t* books_f16, void* stream);
+
 /* Static description of a status code. */
 const char* fkv_status_string(int status);
 

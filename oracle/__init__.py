@@ -74,6 +74,9 @@ def _load():
     lib.fkvo_suffix_search.argtypes = [c_i32, c_dbl, c_p, c_p, c_p, c_i64, c_i64, c_p, c_i32, c_i32, c_p,
                                        c_i64, c_p]
     lib.fkvo_suffix_search.restype = c_i64
+    lib.fkvo_kmeans_update.argtypes = [c_i64, c_i64, c_i64, c_i64, c_i32, c_i32, c_i32, c_i32, c_p, c_p, c_p,
+                                       c_p, c_i32, c_p, c_p]
+    lib.fkvo_kmeans_update.restype = None
     _lib = lib
     return lib
 
@@ -282,3 +285,27 @@ def suffix_search(codec: Codec, traj: np.ndarray, query: np.ndarray, verify: boo
     nh = _load().fkvo_suffix_search(codec.N, codec.r, _ptr(codec.V), _ptr(codec.W), _ptr(tr), ns, n, _ptr(q),
                                     q.size, 1 if verify else 0, _ptr(hits), max_hits, _ptr(nc))
     return hits[:min(nh, max_hits)], int(nh), int(nc[0])
+
+
+def kmeans_update(x_f16: np.ndarray, books_f16: np.ndarray, stream_book: np.ndarray, t_begin: int, t_end: int,
+                  symbols: np.ndarray, stage: int):
+    """One Lloyd update of residual stage `stage` (Sec. 3 "Setup": codebooks trained by k-means).
+
+    -> (new books f16 [n_books][S][K][d] with stage `stage` replaced by the cluster means rounded to
+    binary16 (round to nearest even; an empty cluster keeps its centroid), means f64
+    [n_books][K][d], counts i64 [n_books][K])."""
+    x = np.ascontiguousarray(x_f16, dtype=np.float16)
+    bk = np.ascontiguousarray(books_f16, dtype=np.float16)
+    sb = np.ascontiguousarray(stream_book, dtype=np.int32)
+    ns, T, d = x.shape
+    nb, S, K, d2 = bk.shape
+    assert d2 == d and 0 <= stage < S
+    Ta = t_end - t_begin
+    sym = np.ascontiguousarray(symbols, dtype=np.uint8).reshape(ns, Ta * S)
+    means = np.zeros((nb, K, d), np.float64)
+    counts = np.zeros((nb, K), np.int64)
+    _load().fkvo_kmeans_update(ns, T, t_begin, t_end, d, S, K, nb, _ptr(x.view(np.uint16)), _ptr(bk.view(np.uint16)),
+                               _ptr(sb), _ptr(sym), stage, _ptr(means), _ptr(counts))
+    new = bk.copy()
+    new[:, stage] = means.astype(np.float16)
+    return new, means, counts

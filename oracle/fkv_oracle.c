@@ -511,3 +511,55 @@ int64_t fkvo_suffix_search(int32_t N, double r, const double* V, const double* W
     if (n_candidates) *n_candidates = n_cand;
     return n_hit;
 }
+
+/* ---------------------------------------------------------------- k-means -- */
+
+/*
+ * Sec. 3 ("Setup"): codebooks are trained by k-means.  One Lloyd update of
+ * residual stage `stage` of per-head books: every archived token t of every
+ * stream contributes its stage input r = x_t - sum_{st<stage} C[b][st][i_st]
+ * to cluster i_stage of its book b = stream_book[s]; the new centroid of a
+ * cluster is the mean of its members, and an empty cluster keeps its
+ * centroid.  Sums are exact integers in units of 2^-24 (every binary16 value
+ * is a multiple of 2^-24); mean = (double)sum / count * 2^-24.
+ *   means:  out [n_books][K][d] (the old centroid where count == 0)
+ *   counts: out [n_books][K]
+ */
+void fkvo_kmeans_update(int64_t n_streams, int64_t T, int64_t t_begin, int64_t t_end, int32_t d,
+                        int32_t S, int32_t K, int32_t n_books, const uint16_t* x, const uint16_t* books,
+                        const int32_t* stream_book, const uint8_t* symbols, int32_t stage,
+                        double* means, int64_t* counts)
+{
+    int64_t Ta = t_end - t_begin;
+    int64_t* sums = (int64_t*)calloc((size_t)n_books * K * d, sizeof(int64_t));
+    for (int64_t i = 0; i < (int64_t)n_books * K; ++i) counts[i] = 0;
+    for (int64_t s = 0; s < n_streams; ++s) {
+        int32_t b = stream_book[s];
+        if (b < 0 || b >= n_books) continue;
+        const uint16_t* book = books + (int64_t)b * S * K * d;
+        for (int64_t t = 0; t < Ta; ++t) {
+            const uint8_t* sym = symbols + (s * Ta + t) * S;
+            int32_t j = sym[stage], bad = 0;
+            for (int32_t st = 0; st <= stage; ++st)
+                if (sym[st] >= K) bad = 1;
+            if (bad) continue; /* a symbol outside the book: the token is skipped */
+            const uint16_t* xv = x + (s * T + t_begin + t) * d;
+            for (int32_t e = 0; e < d; ++e) {
+                double r = fkvo_half_to_double(xv[e]);
+                for (int32_t st = 0; st < stage; ++st)
+                    r = r - fkvo_half_to_double(book[((int64_t)st * K + sym[st]) * d + e]);
+                sums[((int64_t)b * K + j) * d + e] += (int64_t)ldexp(r, 24); /* exact */
+            }
+            counts[(int64_t)b * K + j] += 1;
+        }
+    }
+    for (int64_t b = 0; b < n_books; ++b)
+        for (int32_t j = 0; j < K; ++j)
+            for (int32_t e = 0; e < d; ++e) {
+                int64_t c = counts[b * K + j];
+                double m = c ? ldexp((double)sums[(b * K + j) * d + e] / (double)c, -24)
+                             : fkvo_half_to_double(books[(((int64_t)b * S + stage) * K + j) * d + e]);
+                means[(b * K + j) * d + e] = m;
+            }
+    free(sums);
+}

@@ -21,21 +21,6 @@ namespace {
 
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 
-// Correctly rounded binary64 -> binary16 (round to nearest, ties to even): the
-// conversion to binary32 is made round-to-odd (truncate, then set the last
-// bit when inexact), which carries enough information for the final
-// round-to-nearest-even step to binary16 (binary32 has 13 more bits).
-__device__ inline _Float16 f64_to_f16(double v)
-{
-    const float f = (float)v;
-    uint32_t u = __float_as_uint(f);
-    if ((double)f != v) {
-        if (fabs((double)f) > fabs(v)) u -= 1;   // towards zero
-        u |= 1u;
-    }
-    return (_Float16)__uint_as_float(u);
-}
-
 // ---------------------------------------------------------------- rehydrate --
 
 template <bool EXACT>

@@ -60,6 +60,21 @@ __device__ inline void lds_to_bytes(const uint8_t* lds, int64_t g0, int64_t g1,
     if (tid < g1 - a1) dst[a1 + tid] = lds[a1 + tid - base];
 }
 
+// Correctly rounded binary64 -> binary16 (round to nearest, ties to even): the
+// conversion to binary32 is made round-to-odd (truncate, then set the last
+// bit when inexact), which carries enough information for the final
+// round-to-nearest-even step to binary16 (binary32 has 13 more bits).
+__device__ inline _Float16 f64_to_f16(double v)
+{
+    const float f = (float)v;
+    uint32_t u = __float_as_uint(f);
+    if ((double)f != v) {
+        if (fabs((double)f) > fabs(v)) u -= 1;   // towards zero
+        u |= 1u;
+    }
+    return (_Float16)__uint_as_float(u);
+}
+
 // Adds the number of lanes of the block with `flag` set to *counter, one
 // atomic per wave that has any.
 __device__ inline void count_flags(bool flag, uint32_t* counter)

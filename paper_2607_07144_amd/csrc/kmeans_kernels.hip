@@ -1,0 +1,119 @@
+// kmeans_kernels.hip -- one Lloyd update of a residual stage of per-head
+// codebooks (Sec. 3 "Setup": codebooks are trained by k-means), for gfx950.
+//
+// The assignment step is fkv_rvq_assign.  Accumulate: one lane per 8
+// dimensions of one archived token forms the stage input r = x - (codewords of
+// the earlier stages) exactly in fp64 and adds it, as an integer in units of
+// 2^-24 (every binary16 value is a multiple of 2^-24), to its cluster's sum with
+// 64-bit atomics -- integer addition, so the sums do not depend on the order
+// of the atomics.  Finalize: mean = sum / count * 2^-24 in fp64, rounded once to
+// binary16; an empty cluster keeps its centroid.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "fkv.h"
+#include "fkv_hip_common.h"
+
+#pragma clang fp contract(off)
+
+namespace fkv {
+namespace {
+
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+constexpr int kThreads = 256;
+
+__global__ __launch_bounds__(kThreads) void kmeans_accumulate_kernel(
+    const _Float16* __restrict__ x, const _Float16* __restrict__ books, const int32_t* __restrict__ stream_book,
+    const uint8_t* __restrict__ symbols, unsigned long long* __restrict__ sums, uint32_t* __restrict__ counts,
+    int64_t T, int64_t t_begin, int64_t Ta, int d, int S, int K, int n_books, int stage, int64_t n_tasks)
+{
+    const int nch = d / 8;
+    for (int64_t task = (int64_t)blockIdx.x * kThreads + threadIdx.x; task < n_tasks;
+         task += (int64_t)gridDim.x * kThreads) {
+        const int64_t tok = task / nch;   // stream * Ta + t
+        const int ch = (int)(task - tok * nch);
+        const int64_t s = tok / Ta, t = tok - s * Ta;
+        const int b = stream_book[s];
+        if (b < 0 || b >= n_books) continue;
+        const uint8_t* sym = symbols + tok * S;
+        bool bad = false;
+        for (int st = 0; st <= stage; ++st) bad = bad || sym[st] >= K;
+        if (bad) continue;   // a symbol outside the book: the token is skipped
+        const half8 xv = *(const half8*)(x + (s * T + t_begin + t) * d + ch * 8);
+        double r[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) r[e] = (double)xv[e];
+        for (int st = 0; st < stage; ++st) {
+            const half8 c = *(const half8*)(books + (((int64_t)b * S + st) * K + sym[st]) * d + ch * 8);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) r[e] = r[e] - (double)c[e];
+        }
+        unsigned long long* dst = sums + ((int64_t)b * K + sym[stage]) * d + ch * 8;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) atomicAdd(dst + e, (unsigned long long)(long long)ldexp(r[e], 24));
+        if (ch == 0) atomicAdd(counts + (int64_t)b * K + sym[stage], 1u);
+    }
+}
+
+__global__ __launch_bounds__(kThreads) void kmeans_finalize_kernel(
+    const unsigned long long* __restrict__ sums, const uint32_t* __restrict__ counts, _Float16* __restrict__ books,
+    int d, int S, int K, int stage, int64_t n_elems)
+{
+    for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n_elems; i += (int64_t)gridDim.x * kThreads) {
+        const int64_t bj = i / d;   // book * K + j
+        const int e = (int)(i - bj * d);
+        const uint32_t c = counts[bj];
+        if (c == 0) continue;
+        const int64_t b = bj / K, j = bj - b * K;
+        const double m = ldexp((double)(long long)sums[i] / (double)c, -24);
+        books[((b * S + stage) * K + j) * d + e] = f64_to_f16(m);
+    }
+}
+
+int64_t grid_for(int64_t n)
+{
+    const int64_t b = (n + kThreads - 1) / kThreads;
+    return b < 1 ? 1 : (b > 4096 ? 4096 : b);
+}
+
+}  // namespace
+}  // namespace fkv
+
+using namespace fkv;
+
+extern "C" int fkv_kmeans_accumulate(const fkv_rvq_desc* desc, const uint16_t* x_f16, const uint16_t* books_f16,
+                                     const int32_t* stream_book, const uint8_t* symbols, int32_t stage,
+                                     int64_t* sums, uint32_t* counts, void* stream)
+{
+    if (!desc) return FKV_ERR_INVALID_ARG;
+    const fkv_rvq_desc& D = *desc;
+    if (D.n_streams < 0 || D.T < 0 || D.t_begin < 0 || D.t_end < D.t_begin || D.t_end > D.T) return FKV_ERR_INVALID_ARG;
+    if (D.d < 8 || D.d > 256 || D.d % 8 != 0 || D.S < 1 || D.S > 8 || D.K < 1 || D.K > 256 || D.n_books < 1)
+        return FKV_ERR_INVALID_ARG;
+    if (stage < 0 || stage >= D.S) return FKV_ERR_INVALID_ARG;
+    const int64_t Ta = D.t_end - D.t_begin;
+    if (D.n_streams == 0 || Ta == 0) return FKV_OK;
+    if (!x_f16 || !books_f16 || !stream_book || !symbols || !sums || !counts) return FKV_ERR_INVALID_ARG;
+    if (!aligned(x_f16, 16) || !aligned(books_f16, 16) || !aligned(sums, 8) || !aligned(counts, 4) ||
+        !aligned(stream_book, 4))
+        return FKV_ERR_INVALID_ARG;
+    const int64_t n_tasks = D.n_streams * Ta * (D.d / 8);
+    hipLaunchKernelGGL(kmeans_accumulate_kernel, dim3((unsigned)grid_for(n_tasks)), dim3(kThreads), 0,
+                       (hipStream_t)stream, (const _Float16*)x_f16, (const _Float16*)books_f16, stream_book, symbols,
+                       (unsigned long long*)sums, counts, D.T, D.t_begin, Ta, D.d, D.S, D.K, D.n_books, stage, n_tasks);
+    return launch_status();
+}
+
+extern "C" int fkv_kmeans_finalize(int32_t n_books, int32_t S, int32_t K, int32_t d, int32_t stage,
+                                   const int64_t* sums, const uint32_t* counts, uint16_t* books_f16, void* stream)
+{
+    if (n_books < 1 || S < 1 || S > 8 || K < 1 || K > 256 || d < 8 || d > 256 || d % 8 != 0) return FKV_ERR_INVALID_ARG;
+    if (stage < 0 || stage >= S || !sums || !counts || !books_f16) return FKV_ERR_INVALID_ARG;
+    if (!aligned(sums, 8) || !aligned(counts, 4) || !aligned(books_f16, 2)) return FKV_ERR_INVALID_ARG;
+    const int64_t n_elems = (int64_t)n_books * K * d;
+    hipLaunchKernelGGL(kmeans_finalize_kernel, dim3((unsigned)grid_for(n_elems)), dim3(kThreads), 0,
+                       (hipStream_t)stream, (const unsigned long long*)sums, counts, (_Float16*)books_f16, d, S, K,
+                       stage, n_elems);
+    return launch_status();
+}

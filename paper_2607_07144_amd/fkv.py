@@ -52,6 +52,8 @@ _SIGS = {
     "fkv_cgr_append": ([_PC, _p, _p, _i64, _i64, _i64, _p, _i64, _p], ctypes.c_int),
     "fkv_trajectory": ([_PC, _p, _p, _i64, _i64, _i32, _p, _p], ctypes.c_int),
     "fkv_suffix_search": ([_PC, _p, _p, _i64, _i64, _p, _i32, _i32, _p, _i64, _p, _p, _p], ctypes.c_int),
+    "fkv_kmeans_accumulate": ([ctypes.POINTER(fkv_rvq_desc), _p, _p, _p, _p, _i32, _p, _p, _p], ctypes.c_int),
+    "fkv_kmeans_finalize": ([_i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p], ctypes.c_int),
     "fkv_status_string": ([ctypes.c_int], ctypes.c_char_p),
     "fkv_version": ([], ctypes.c_char_p),
 }
@@ -312,6 +314,39 @@ def fkv_suffix_search(codec: Codec, traj, query, verify: bool = True, max_hits: 
                                  _ptr(query), query.numel(), 1 if verify else 0, _ptr(hits), max_hits,
                                  _ptr(n_hits), _ptr(n_candidates), _stream(stream)), "fkv_suffix_search")
     return hits, n_hits, n_candidates
+
+
+# ------------------------------------------------------------------ k-means
+
+def fkv_kmeans_step(x, books, stream_book, t_begin: int, t_end: int, symbols, stage: int, sums=None, counts=None,
+                    stream=None):
+    """One Lloyd update of stage `stage` of `books` (in place) from an assignment `symbols`;
+    returns (books, counts).  sums int64 [n_books][K][d] and counts int32 [n_books][K] are
+    workspace (zeroed here)."""
+    torch = _torch()
+    _need(x, torch.float16, "x")
+    _need(books, torch.float16, "books")
+    _need(stream_book, torch.int32, "stream_book")
+    _need(symbols, torch.uint8, "symbols")
+    ns, T, d = x.shape
+    nb, S, K, d2 = books.shape
+    if d2 != d or stream_book.shape != (ns,) or symbols.numel() != ns * (t_end - t_begin) * S:
+        raise ValueError("shape mismatch")
+    if sums is None:
+        sums = torch.zeros((nb, K, d), dtype=torch.int64, device=x.device)
+    else:
+        sums.zero_()
+    if counts is None:
+        counts = torch.zeros((nb, K), dtype=torch.int32, device=x.device)
+    else:
+        counts.zero_()
+    desc = fkv_rvq_desc(ns, T, t_begin, t_end, d, S, K, nb)
+    st = _stream(stream)
+    _check(lib.fkv_kmeans_accumulate(ctypes.byref(desc), _ptr(x), _ptr(books), _ptr(stream_book), _ptr(symbols),
+                                     stage, _ptr(sums), _ptr(counts), st), "fkv_kmeans_accumulate")
+    _check(lib.fkv_kmeans_finalize(nb, S, K, d, stage, _ptr(sums), _ptr(counts), _ptr(books), st),
+           "fkv_kmeans_finalize")
+    return books, counts
 
 
 def fkv_version() -> str:
