@@ -191,6 +191,22 @@ def next_rows(fkv, cfg, groups, side, replays: int):
 
             res["evict_append"]["s"] += time_graph(step, 10, replays, side)
             res["evict_append"]["bytes"] += ns * (cfg.d * 2 + g.S) + gr["books"].numel() * 2 + ns * 32
+            # one Lloyd iteration of codebook training over every stage (assign, accumulate, update)
+            bk = gr["books"].clone()
+            nb, S, K = bk.shape[0], bk.shape[1], bk.shape[2]
+            symk = torch.empty_like(gr["sym"])
+            sums = torch.zeros((nb, K, cfg.d), dtype=torch.int64, device="cuda")
+            counts = torch.zeros((nb, K), dtype=torch.int32, device="cuda")
+
+            def lloyd():
+                for stage in range(S):
+                    fkv.fkv_rvq_assign(gr["x"], bk, gr["sb"], cfg.t_begin, cfg.t_end, symbols=symk)
+                    fkv.fkv_kmeans_step(gr["x"], bk, gr["sb"], cfg.t_begin, cfg.t_end, symk, stage, sums=sums,
+                                        counts=counts)
+
+            res.setdefault("kmeans", {"s": 0.0, "books": 0})
+            res["kmeans"]["s"] += time_graph(lloyd, 2, replays, side)
+            res["kmeans"]["books"] += nb
     rh, ev = res["rehydrate"], res["evict_append"]
     ach = rh["bytes"] / rh["s"] / 1e9
     return {
@@ -201,6 +217,9 @@ def next_rows(fkv, cfg, groups, side, replays: int):
         "evict_append": {"us_per_decoding_step": round(ev["s"] * 1e6, 2),
                          "positions_per_s": round(1.0 / ev["s"], 1),
                          "streams": sum(gr["ns"] for gr in groups)},
+        "kmeans": {"ms_per_lloyd_iteration": round(res["kmeans"]["s"] * 1e3, 4),
+                   "books": res["kmeans"]["books"],
+                   "note": "every stage: assignment, cluster sums, centroid update"},
     }
 
 
