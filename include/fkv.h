@@ -119,6 +119,22 @@ int fkv_rvq_assign(const fkv_rvq_desc* desc, const uint16_t* x_f16, const uint16
                    const int32_t* stream_book, uint8_t* symbols, float* residual,
                    uint32_t* n_bad_streams, void* stream);
 
+/* ---- a2 + a3 fused: assignment and span encode in one kernel --------------
+ * Equivalent to fkv_rvq_assign followed by fkv_cgr_encode_spans of its
+ * symbols (n_sym = (t_end - t_begin) * S per stream): the same symbols and the
+ * same points, bit for bit.  Each assignment block takes a token range that
+ * holds whole spans (a multiple of L / gcd(L, S) tokens) and encodes them as
+ * soon as its last stage is assigned, so the symbols are never read back.
+ *   c, dev_table  the codec, as for fkv_cgr_encode_spans
+ *   points        device f64 [n_streams][n_spans][2] (n_spans = ceil(n_sym / L)),
+ *                 16-byte aligned; a stream with an invalid book id gets NaN
+ *                 points, as encoding its 0xFF symbols would give
+ * The other arguments are those of fkv_rvq_assign. */
+int fkv_rvq_assign_encode(const fkv_rvq_desc* desc, const uint16_t* x_f16, const uint16_t* books_f16,
+                          const int32_t* stream_book, const fkv_codec* c, const void* dev_table,
+                          uint8_t* symbols, double* points, float* residual, uint32_t* n_bad_streams,
+                          void* stream);
+
 /* ---- a3: fixed-span chaos-game encode (Sec. 1 "The code", Sec. 2) --------
  * symbols [n_streams][n_sym] (device u8) -> points [n_streams][n_spans][2]
  * (device f64, x then y; 16-byte aligned), n_spans = fkv_num_spans().

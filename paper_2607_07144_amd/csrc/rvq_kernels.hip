@@ -48,6 +48,7 @@
 
 #include "fkv.h"
 #include "fkv_hip_common.h"
+#include "fkv_internal.h"
 
 namespace fkv {
 namespace {
@@ -326,7 +327,8 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
     const _Float16* __restrict__ x, const _Float16* __restrict__ books,
     const int32_t* __restrict__ stream_book, uint8_t* __restrict__ symbols,
     float* __restrict__ residual, uint32_t* __restrict__ n_bad, int64_t T, int64_t t_begin,
-    int64_t Ta, int S, int K, int Kp, int n_books, int64_t blocks_per_stream)
+    int64_t Ta, int S, int K, int Kp, int n_books, int64_t blocks_per_stream, int64_t tpb,
+    double2* __restrict__ points, const double2* __restrict__ vtab, double cr, int cN, int cL, int64_t n_spans)
 {
     using C = Cfg<D>;
     constexpr int KS = C::KS, TT = C::TT, TOK = C::TOK, NBUF = C::NBUF;
@@ -341,7 +343,8 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
     const uint32_t xcd = blockIdx.x % 8, slot = blockIdx.x / 8;
     const int64_t item = (int64_t)xcd * q8 + min(xcd, r8) + slot;
     const int64_t s = item / blocks_per_stream;
-    const int64_t tb = (item - s * blocks_per_stream) * TOK;
+    const int64_t tb = (item - s * blocks_per_stream) * tpb;   // first token of the block
+    const int64_t te = min(Ta, tb + tpb);                      // one past its last
 
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int col = lane & 31, hh = lane >> 5;
@@ -356,7 +359,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
 #pragma unroll
     for (int tt = 0; tt < TT; ++tt) {
         tok[tt] = tb + (int64_t)(wave * TT + tt) * 32 + col;
-        valid[tt] = tok[tt] < Ta;
+        valid[tt] = tok[tt] < te;
         const _Float16* row = x + (s * T + t_begin + (valid[tt] ? tok[tt] : 0)) * D + 8 * hh;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
@@ -366,14 +369,22 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
     }
 
     if (b < 0 || b >= n_books) {
-        const int64_t te = min(Ta, tb + TOK);
         for (int64_t i = tb * S + tid; i < te * S; i += C::THREADS) sym_s[i] = 0xFF;
+        if (points)   // the block's spans encode 0xFF symbols: NaN points, as a separate encode gives
+            for (int64_t j = tb * S / cL + tid; j < (te * S + cL - 1) / cL; j += C::THREADS)
+                points[s * n_spans + j] = make_double2(NAN, NAN);
         if (residual)
             for (int64_t i = tb * D + tid; i < te * D; i += C::THREADS) residual[s * Ta * D + i] = NAN;
         if (tid == 0 && tb == 0 && n_bad) atomicAdd(n_bad, 1u);
         return;
     }
     const _Float16* bk = books + (int64_t)b * S * K * D;
+
+    // Fused span encode: the vertex table (NaN beyond the alphabet) and the
+    // block's symbols live after the book buffers.
+    double2* V_l = (double2*)(lds + NBUF * buf_bytes);
+    uint8_t* sym_l = (uint8_t*)(V_l + 256);
+    if (points && tid < 256) V_l[tid] = tid < cN ? vtab[tid] : make_double2(NAN, NAN);
 
     // start the first books' copies; zero the buffers' end pads
     book_to_lds_async<D>(bk, K, Kp, lds, wave, lane);
@@ -431,7 +442,10 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
                 val = oval;
                 cw = ocw;
             }
-            if (hh == 0 && valid[tt]) sym_s[tok[tt] * S + st] = (uint8_t)cw;
+            if (hh == 0 && valid[tt]) {
+                sym_s[tok[tt] * S + st] = (uint8_t)cw;
+                if (points) sym_l[(tok[tt] - tb) * S + st] = (uint8_t)cw;
+            }
             // next stage's bias: this stage's winning |u| grown by 2^-10
             bz[tt] = bias_column(-__uint_as_float(val) * (1.0f + 0x1p-10f), hh);
             // this lane's chunks of the chosen codeword
@@ -489,49 +503,106 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
             __syncthreads();
         }
     }
+    if (points) {
+        // Span encode of the block's symbols (Sec. 1 "The code"): the block's
+        // token range holds whole spans, each walked from the anchor (0,0) with
+        // p <- V + r (p - V), operation for operation as the encode kernel.
+        __syncthreads();
+        const int64_t n_sym = Ta * S;
+        for (int64_t j = tb * S / cL + tid; j < (te * S + cL - 1) / cL; j += C::THREADS) {
+            const int64_t a = j * cL;
+            const int len = (int)min((int64_t)cL, n_sym - a);
+            const uint8_t* my = sym_l + (a - tb * S);
+            double px = 0.0, py = 0.0;
+            for (int k0 = 0; k0 < len; k0 += 8) {
+                // the vertices of up to 8 symbols first (they do not depend on p),
+                // then the dependent steps
+                double2 v[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) v[u] = k0 + u < len ? V_l[my[k0 + u]] : make_double2(0.0, 0.0);
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    if (k0 + u < len) {
+                        const double tx = px - v[u].x, ty = py - v[u].y;
+                        const double ux = cr * tx, uy = cr * ty;
+                        px = v[u].x + ux;
+                        py = v[u].y + uy;
+                    }
+                }
+            }
+            points[s * n_spans + j] = make_double2(px, py);
+        }
+    }
 }
+
+// LDS after the book buffers for the fused span encode: 256 vertices and the
+// block's symbols.
+template <int D>
+constexpr size_t enc_lds_bytes()
+{
+    return 256 * 16 + (size_t)Cfg<D>::TOK * 8;
+}
+
+// Fused encode parameters (points == nullptr: assignment only).
+struct EncArgs {
+    double2* points;
+    const double2* vtab;
+    double r;
+    int N, L;
+};
 
 template <int D, bool HILO>
 int launch_rvq_t(const fkv_rvq_desc* dsc, const uint16_t* x, const uint16_t* books,
                  const int32_t* stream_book, uint8_t* symbols, float* residual, uint32_t* n_bad,
-                 hipStream_t stream)
+                 const EncArgs& enc, hipStream_t stream)
 {
     static std::once_flag once;
     const int Kp = (dsc->K + 63) / 64 * 64;  // whole pairs of 32-codeword tiles
     std::call_once(once, [] {
         (void)hipFuncSetAttribute((const void*)rvq_assign_kernel<D, HILO>,
-                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes<D>(256));
+                                  hipFuncAttributeMaxDynamicSharedMemorySize,
+                                  (int)(lds_bytes<D>(256) + enc_lds_bytes<D>()));
     });
     (void)hipGetLastError();
     const int64_t Ta = dsc->t_end - dsc->t_begin;
-    const int64_t bps = (Ta + Cfg<D>::TOK - 1) / Cfg<D>::TOK;
+    // Tokens per block: with the fused encode, a multiple of L / gcd(L, S) so
+    // that every block holds whole spans.
+    int64_t tpb = Cfg<D>::TOK;
+    if (enc.points) {
+        int a = enc.L, b = dsc->S;
+        while (b) {
+            const int t = a % b;
+            a = b;
+            b = t;
+        }
+        const int unit = enc.L / a;
+        tpb = (int64_t)(Cfg<D>::TOK / unit) * unit;
+    }
+    const int64_t bps = (Ta + tpb - 1) / tpb;
     const int64_t nblk = bps * dsc->n_streams;
     if (nblk > 0x7fffffff) return FKV_ERR_UNSUPPORTED;
-    hipLaunchKernelGGL((rvq_assign_kernel<D, HILO>), dim3((unsigned)nblk), dim3(Cfg<D>::THREADS),
-                       lds_bytes<D>(Kp), stream, (const _Float16*)x, (const _Float16*)books, stream_book,
-                       symbols, residual, n_bad, dsc->T, dsc->t_begin, Ta, dsc->S, dsc->K, Kp,
-                       dsc->n_books, bps);
+    const int64_t n_spans = enc.points ? (Ta * dsc->S + enc.L - 1) / enc.L : 0;
+    const size_t shm = lds_bytes<D>(Kp) + (enc.points ? enc_lds_bytes<D>() : 0);
+    hipLaunchKernelGGL((rvq_assign_kernel<D, HILO>), dim3((unsigned)nblk), dim3(Cfg<D>::THREADS), shm, stream,
+                       (const _Float16*)x, (const _Float16*)books, stream_book, symbols, residual, n_bad, dsc->T,
+                       dsc->t_begin, Ta, dsc->S, dsc->K, Kp, dsc->n_books, bps, tpb, enc.points, enc.vtab, enc.r,
+                       enc.N, enc.L, n_spans);
     return launch_status();
 }
 
 template <int D>
 int launch_rvq(const fkv_rvq_desc* dsc, const uint16_t* x, const uint16_t* books,
                const int32_t* stream_book, uint8_t* symbols, float* residual, uint32_t* n_bad,
-               hipStream_t stream)
+               const EncArgs& enc, hipStream_t stream)
 {
     if (dsc->S <= 2)
-        return launch_rvq_t<D, false>(dsc, x, books, stream_book, symbols, residual, n_bad, stream);
-    return launch_rvq_t<D, true>(dsc, x, books, stream_book, symbols, residual, n_bad, stream);
+        return launch_rvq_t<D, false>(dsc, x, books, stream_book, symbols, residual, n_bad, enc, stream);
+    return launch_rvq_t<D, true>(dsc, x, books, stream_book, symbols, residual, n_bad, enc, stream);
 }
 
-}  // namespace
-}  // namespace fkv
-
-using namespace fkv;
-
-extern "C" int fkv_rvq_assign(const fkv_rvq_desc* desc, const uint16_t* x_f16, const uint16_t* books_f16,
-                              const int32_t* stream_book, uint8_t* symbols, float* residual,
-                              uint32_t* n_bad_streams, void* stream)
+int rvq_dispatch(const fkv_rvq_desc* desc, const uint16_t* x_f16, const uint16_t* books_f16,
+                 const int32_t* stream_book, uint8_t* symbols, float* residual, uint32_t* n_bad_streams,
+                 const EncArgs& enc, void* stream)
 {
     if (!desc) return FKV_ERR_INVALID_ARG;
     const fkv_rvq_desc& d = *desc;
@@ -547,7 +618,7 @@ extern "C" int fkv_rvq_assign(const fkv_rvq_desc* desc, const uint16_t* x_f16, c
     if (n_bad_streams && !aligned(n_bad_streams, 4)) return FKV_ERR_INVALID_ARG;
     const hipStream_t st = (hipStream_t)stream;
 #define FKV_RVQ_CASE(DD) \
-    case DD: return launch_rvq<DD>(desc, x_f16, books_f16, stream_book, symbols, residual, n_bad_streams, st);
+    case DD: return launch_rvq<DD>(desc, x_f16, books_f16, stream_book, symbols, residual, n_bad_streams, enc, st);
     switch (d.d) {
         FKV_RVQ_CASE(16) FKV_RVQ_CASE(32) FKV_RVQ_CASE(48) FKV_RVQ_CASE(64)
         FKV_RVQ_CASE(80) FKV_RVQ_CASE(96) FKV_RVQ_CASE(112) FKV_RVQ_CASE(128)
@@ -556,4 +627,29 @@ extern "C" int fkv_rvq_assign(const fkv_rvq_desc* desc, const uint16_t* x_f16, c
     default: return FKV_ERR_INVALID_ARG;
     }
 #undef FKV_RVQ_CASE
+}
+
+}  // namespace
+}  // namespace fkv
+
+using namespace fkv;
+
+extern "C" int fkv_rvq_assign(const fkv_rvq_desc* desc, const uint16_t* x_f16, const uint16_t* books_f16,
+                              const int32_t* stream_book, uint8_t* symbols, float* residual,
+                              uint32_t* n_bad_streams, void* stream)
+{
+    const EncArgs none = {nullptr, nullptr, 0.0, 0, 1};
+    return rvq_dispatch(desc, x_f16, books_f16, stream_book, symbols, residual, n_bad_streams, none, stream);
+}
+
+extern "C" int fkv_rvq_assign_encode(const fkv_rvq_desc* desc, const uint16_t* x_f16, const uint16_t* books_f16,
+                                     const int32_t* stream_book, const fkv_codec* c, const void* dev_table,
+                                     uint8_t* symbols, double* points, float* residual, uint32_t* n_bad_streams,
+                                     void* stream)
+{
+    if (!c || c->N < 3 || c->N > 256 || c->L < 1 || c->L > 64 || !(c->r > 0.0 && c->r < 1.0)) return FKV_ERR_INVALID_ARG;
+    if (!dev_table || !points || !aligned(dev_table, 16) || !aligned(points, 16)) return FKV_ERR_INVALID_ARG;
+    const EncArgs enc = {(double2*)points, (const double2*)((const uint8_t*)dev_table + table_off_V(c->N)), c->r,
+                         c->N, c->L};
+    return rvq_dispatch(desc, x_f16, books_f16, stream_book, symbols, residual, n_bad_streams, enc, stream);
 }

@@ -44,6 +44,8 @@ _SIGS = {
     "fkv_codec_fill_table": ([_PC, _p], ctypes.c_int),
     "fkv_num_spans": ([_PC, _i64], _i64),
     "fkv_rvq_assign": ([ctypes.POINTER(fkv_rvq_desc), _p, _p, _p, _p, _p, _p, _p], ctypes.c_int),
+    "fkv_rvq_assign_encode": ([ctypes.POINTER(fkv_rvq_desc), _p, _p, _p, _PC, _p, _p, _p, _p, _p, _p],
+                              ctypes.c_int),
     "fkv_cgr_encode_spans": ([_PC, _p, _p, _i64, _i64, _p, _p], ctypes.c_int),
     "fkv_cgr_decode_spans": ([_PC, _p, _p, _i64, _i64, _p, _p, _p, _i32, _p], ctypes.c_int),
     "fkv_span_lookup": ([_PC, _p, _p, _i64, _i64, _i32, _p, _p, _i64, _p, _p, _p, _p], ctypes.c_int),
@@ -163,6 +165,44 @@ def fkv_rvq_assign(x, books, stream_book, t_begin: int, t_end: int, symbols=None
     _check(lib.fkv_rvq_assign(ctypes.byref(desc), _ptr(x), _ptr(books), _ptr(stream_book), _ptr(symbols),
                               _ptr(residual), _ptr(n_bad), _stream(stream)), "fkv_rvq_assign")
     return symbols, residual
+
+
+def fkv_rvq_assign_encode(codec: Codec, x, books, stream_book, t_begin: int, t_end: int, symbols=None, points=None,
+                          residual=None, want_residual: bool = False, n_bad=None, stream=None):
+    """Assignment and span encode in one kernel: returns (symbols, points, residual or None), identical to
+    fkv_rvq_assign followed by fkv_cgr_encode_spans."""
+    torch = _torch()
+    _need(x, torch.float16, "x")
+    _need(books, torch.float16, "books")
+    _need(stream_book, torch.int32, "stream_book")
+    ns, T, d = x.shape
+    nb, S, K, d2 = books.shape
+    if d2 != d or stream_book.shape != (ns,):
+        raise ValueError("shape mismatch between x, books and stream_book")
+    Ta = t_end - t_begin
+    if symbols is None:
+        symbols = torch.empty((ns, Ta * S), dtype=torch.uint8, device=x.device)
+    _need(symbols, torch.uint8, "symbols")
+    if symbols.numel() != ns * Ta * S:
+        raise ValueError("symbols has the wrong size")
+    n_spans = codec.n_spans(Ta * S)
+    if points is None:
+        points = torch.empty((ns, n_spans, 2), dtype=torch.float64, device=x.device)
+    _need(points, torch.float64, "points")
+    if points.numel() != ns * n_spans * 2:
+        raise ValueError("points has the wrong size")
+    if residual is None and want_residual:
+        residual = torch.empty((ns, Ta, d), dtype=torch.float32, device=x.device)
+    if residual is not None:
+        _need(residual, torch.float32, "residual")
+    if n_bad is not None:
+        _need(n_bad, torch.int32, "n_bad")
+    desc = fkv_rvq_desc(ns, T, t_begin, t_end, d, S, K, nb)
+    _check(lib.fkv_rvq_assign_encode(ctypes.byref(desc), _ptr(x), _ptr(books), _ptr(stream_book),
+                                     ctypes.byref(codec.c), _ptr(codec.table(x.device)), _ptr(symbols),
+                                     _ptr(points), _ptr(residual), _ptr(n_bad), _stream(stream)),
+           "fkv_rvq_assign_encode")
+    return symbols, points, residual
 
 
 # ------------------------------------------------------------------ a3: encode

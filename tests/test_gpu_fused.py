@@ -1,0 +1,74 @@
+"""The fused assignment + span encode must reproduce the two separate calls
+exactly: the same symbols, the same points bit for bit, the same residuals,
+for alphabets whose span length divides the token range in different ways
+(L = 16, 9, 6 with S = 2, 3, 4)."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2607_07144_amd import workloads as w
+
+pytestmark = pytest.mark.gpu
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def _compare(fkv, cfg, gi, x, books, sb, sample=None):
+    g = cfg.groups[gi]
+    codec = fkv.Codec(g.N, g.r_scale)
+    sym, res = fkv.fkv_rvq_assign(x, books, sb, cfg.t_begin, cfg.t_end, want_residual=True)
+    pts = fkv.fkv_cgr_encode_spans(codec, sym)
+    fs, fp, fr = fkv.fkv_rvq_assign_encode(codec, x, books, sb, cfg.t_begin, cfg.t_end, want_residual=True)
+    if sample is None:
+        assert torch.equal(fs, sym) and torch.equal(fr, res)
+        assert np.array_equal(host(fp).view(np.uint64), host(pts).view(np.uint64))
+    else:
+        idx = torch.as_tensor(sample, device="cuda")
+        assert torch.equal(fs, sym)
+        assert np.array_equal(host(fp[idx]).view(np.uint64), host(pts[idx]).view(np.uint64))
+        assert torch.equal(fr[idx], res[idx])
+
+
+@pytest.mark.parametrize("name", ["tiny", "gpt2"])
+def test_fused_equals_separate(fkv, name):
+    cfg = w.CONFIGS[name]
+    x, books, sb = (torch.from_numpy(a).cuda() for a in w.make_group_numpy(cfg))
+    _compare(fkv, cfg, 0, x, books, sb)
+
+
+@pytest.mark.parametrize("gi", [0, 1])
+def test_fused_hybrid_groups(fkv, gi):
+    """Keys: S = 4, L = 6 (255-token blocks); values: S = 2, N = 64, L = 9 (252-token blocks)."""
+    cfg = w.CONFIGS["gpt2_hybrid_b16"]
+    x, books, sb = (torch.from_numpy(a).cuda() for a in w.make_group_numpy(cfg, gi))
+    _compare(fkv, cfg, gi, x, books, sb)
+
+
+def test_fused_long_context_sample(fkv):
+    cfg = w.CONFIGS["long_gqa"]
+    x, books, sb = w.make_group_torch(cfg, 0)
+    _compare(fkv, cfg, 0, x, books, sb, sample=[0, 1023, 2047])
+    del x, books, sb
+    torch.cuda.empty_cache()
+
+
+def test_fused_invalid_book_and_ragged(fkv):
+    rng = np.random.default_rng(8)
+    ns, T, d, S, K, N = 5, 300, 32, 3, 40, 64       # L = 9: 9-token units, a ragged last block
+    x = torch.from_numpy(rng.standard_normal((ns, T, d)).astype(np.float16)).cuda()
+    books = torch.from_numpy((rng.standard_normal((2, S, K, d)) * 0.7).astype(np.float16)).cuda()
+    sb = torch.tensor([0, 7, 1, 1, 0], dtype=torch.int32, device="cuda")       # stream 1: invalid book
+    codec = fkv.Codec(N)
+    nb1 = torch.zeros(1, dtype=torch.int32, device="cuda")
+    nb2 = torch.zeros(1, dtype=torch.int32, device="cuda")
+    sym, _ = fkv.fkv_rvq_assign(x, books, sb, 2, 283, n_bad=nb1)
+    pts = fkv.fkv_cgr_encode_spans(codec, sym)
+    fs, fp, _ = fkv.fkv_rvq_assign_encode(codec, x, books, sb, 2, 283, n_bad=nb2)
+    assert torch.equal(fs, sym) and int(nb1.item()) == int(nb2.item()) == 1
+    a, b = host(fp), host(pts)
+    assert np.isnan(a[1]).all() and np.isnan(b[1]).all()
+    keep = [0, 2, 3, 4]
+    assert np.array_equal(a[keep].view(np.uint64), b[keep].view(np.uint64))
