@@ -322,7 +322,7 @@ __device__ __forceinline__ void stage_scan(const uint8_t* buf, uint32_t fa, int 
     pair_second<TT>(acc1, pk, ct >> 1, bkey, bpair);
 }
 
-template <int D, bool HILO>
+template <int D, bool HILO, bool ENC>
 __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assign_kernel(
     const _Float16* __restrict__ x, const _Float16* __restrict__ books,
     const int32_t* __restrict__ stream_book, uint8_t* __restrict__ symbols,
@@ -370,7 +370,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
 
     if (b < 0 || b >= n_books) {
         for (int64_t i = tb * S + tid; i < te * S; i += C::THREADS) sym_s[i] = 0xFF;
-        if (points)   // the block's spans encode 0xFF symbols: NaN points, as a separate encode gives
+        if (ENC)   // the block's spans encode 0xFF symbols: NaN points, as a separate encode gives
             for (int64_t j = tb * S / cL + tid; j < (te * S + cL - 1) / cL; j += C::THREADS)
                 points[s * n_spans + j] = make_double2(NAN, NAN);
         if (residual)
@@ -384,7 +384,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
     // block's symbols live after the book buffers.
     double2* V_l = (double2*)(lds + NBUF * buf_bytes);
     uint8_t* sym_l = (uint8_t*)(V_l + 256);
-    if (points && tid < 256) V_l[tid] = tid < cN ? vtab[tid] : make_double2(NAN, NAN);
+    if (ENC && tid < 256) V_l[tid] = tid < cN ? vtab[tid] : make_double2(NAN, NAN);
 
     // start the first books' copies; zero the buffers' end pads
     book_to_lds_async<D>(bk, K, Kp, lds, wave, lane);
@@ -444,7 +444,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
             }
             if (hh == 0 && valid[tt]) {
                 sym_s[tok[tt] * S + st] = (uint8_t)cw;
-                if (points) sym_l[(tok[tt] - tb) * S + st] = (uint8_t)cw;
+                if (ENC) sym_l[(tok[tt] - tb) * S + st] = (uint8_t)cw;
             }
             // next stage's bias: this stage's winning |u| grown by 2^-10
             bz[tt] = bias_column(-__uint_as_float(val) * (1.0f + 0x1p-10f), hh);
@@ -503,7 +503,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
             __syncthreads();
         }
     }
-    if (points) {
+    if (ENC) {
         // Span encode of the block's symbols (Sec. 1 "The code"): the block's
         // token range holds whole spans, each walked from the anchor (0,0) with
         // p <- V + r (p - V), operation for operation as the encode kernel.
@@ -551,7 +551,7 @@ struct EncArgs {
     int N, L;
 };
 
-template <int D, bool HILO>
+template <int D, bool HILO, bool ENC>
 int launch_rvq_t(const fkv_rvq_desc* dsc, const uint16_t* x, const uint16_t* books,
                  const int32_t* stream_book, uint8_t* symbols, float* residual, uint32_t* n_bad,
                  const EncArgs& enc, hipStream_t stream)
@@ -559,16 +559,16 @@ int launch_rvq_t(const fkv_rvq_desc* dsc, const uint16_t* x, const uint16_t* boo
     static std::once_flag once;
     const int Kp = (dsc->K + 63) / 64 * 64;  // whole pairs of 32-codeword tiles
     std::call_once(once, [] {
-        (void)hipFuncSetAttribute((const void*)rvq_assign_kernel<D, HILO>,
+        (void)hipFuncSetAttribute((const void*)rvq_assign_kernel<D, HILO, ENC>,
                                   hipFuncAttributeMaxDynamicSharedMemorySize,
-                                  (int)(lds_bytes<D>(256) + enc_lds_bytes<D>()));
+                                  (int)(lds_bytes<D>(256) + (ENC ? enc_lds_bytes<D>() : 0)));
     });
     (void)hipGetLastError();
     const int64_t Ta = dsc->t_end - dsc->t_begin;
     // Tokens per block: with the fused encode, a multiple of L / gcd(L, S) so
     // that every block holds whole spans.
     int64_t tpb = Cfg<D>::TOK;
-    if (enc.points) {
+    if (ENC) {
         int a = enc.L, b = dsc->S;
         while (b) {
             const int t = a % b;
@@ -581,9 +581,9 @@ int launch_rvq_t(const fkv_rvq_desc* dsc, const uint16_t* x, const uint16_t* boo
     const int64_t bps = (Ta + tpb - 1) / tpb;
     const int64_t nblk = bps * dsc->n_streams;
     if (nblk > 0x7fffffff) return FKV_ERR_UNSUPPORTED;
-    const int64_t n_spans = enc.points ? (Ta * dsc->S + enc.L - 1) / enc.L : 0;
-    const size_t shm = lds_bytes<D>(Kp) + (enc.points ? enc_lds_bytes<D>() : 0);
-    hipLaunchKernelGGL((rvq_assign_kernel<D, HILO>), dim3((unsigned)nblk), dim3(Cfg<D>::THREADS), shm, stream,
+    const int64_t n_spans = ENC ? (Ta * dsc->S + enc.L - 1) / enc.L : 0;
+    const size_t shm = lds_bytes<D>(Kp) + (ENC ? enc_lds_bytes<D>() : 0);
+    hipLaunchKernelGGL((rvq_assign_kernel<D, HILO, ENC>), dim3((unsigned)nblk), dim3(Cfg<D>::THREADS), shm, stream,
                        (const _Float16*)x, (const _Float16*)books, stream_book, symbols, residual, n_bad, dsc->T,
                        dsc->t_begin, Ta, dsc->S, dsc->K, Kp, dsc->n_books, bps, tpb, enc.points, enc.vtab, enc.r,
                        enc.N, enc.L, n_spans);
@@ -595,9 +595,14 @@ int launch_rvq(const fkv_rvq_desc* dsc, const uint16_t* x, const uint16_t* books
                const int32_t* stream_book, uint8_t* symbols, float* residual, uint32_t* n_bad,
                const EncArgs& enc, hipStream_t stream)
 {
+    if (enc.points) {
+        if (dsc->S <= 2)
+            return launch_rvq_t<D, false, true>(dsc, x, books, stream_book, symbols, residual, n_bad, enc, stream);
+        return launch_rvq_t<D, true, true>(dsc, x, books, stream_book, symbols, residual, n_bad, enc, stream);
+    }
     if (dsc->S <= 2)
-        return launch_rvq_t<D, false>(dsc, x, books, stream_book, symbols, residual, n_bad, enc, stream);
-    return launch_rvq_t<D, true>(dsc, x, books, stream_book, symbols, residual, n_bad, enc, stream);
+        return launch_rvq_t<D, false, false>(dsc, x, books, stream_book, symbols, residual, n_bad, enc, stream);
+    return launch_rvq_t<D, true, false>(dsc, x, books, stream_book, symbols, residual, n_bad, enc, stream);
 }
 
 int rvq_dispatch(const fkv_rvq_desc* desc, const uint16_t* x_f16, const uint16_t* books_f16,
