@@ -72,3 +72,26 @@ def test_fused_invalid_book_and_ragged(fkv):
     assert np.isnan(a[1]).all() and np.isnan(b[1]).all()
     keep = [0, 2, 3, 4]
     assert np.array_equal(a[keep].view(np.uint64), b[keep].view(np.uint64))
+
+
+@pytest.mark.parametrize("d,S,K,N,T", [(16, 1, 16, 16, 400), (48, 3, 64, 64, 333), (128, 2, 256, 256, 700),
+                                       (256, 3, 200, 256, 300), (96, 5, 32, 3, 260), (64, 8, 256, 256, 257)])
+def test_fused_shapes(fkv, d, S, K, N, T):
+    """Random books and inputs over head dims, stage counts and alphabets (L from 6 to 44)."""
+    rng = np.random.default_rng(d + 17 * S + N)
+    ns, nb = 4, 2
+    x = torch.from_numpy(rng.standard_normal((ns, T, d)).astype(np.float16)).cuda()
+    books = torch.from_numpy((rng.standard_normal((nb, S, K, d)) *
+                              (0.5 ** np.arange(S))[None, :, None, None]).astype(np.float16)).cuda()
+    sb = torch.from_numpy(rng.integers(0, nb, ns).astype(np.int32)).cuda()
+    codec = fkv.Codec(N)
+    t0, t1 = 1, T - 2
+    sym, res = fkv.fkv_rvq_assign(x, books, sb, t0, t1, want_residual=True)
+    pts = fkv.fkv_cgr_encode_spans(codec, sym)
+    fs, fp, fr = fkv.fkv_rvq_assign_encode(codec, x, books, sb, t0, t1, want_residual=True)
+    assert torch.equal(fs, sym) and torch.equal(fr, res)
+    a, b = host(fp), host(pts)
+    if K > N:                                       # symbols beyond the alphabet: NaN spans on both sides
+        assert np.array_equal(np.isnan(a), np.isnan(b))
+        a, b = np.nan_to_num(a), np.nan_to_num(b)
+    assert np.array_equal(a.view(np.uint64), b.view(np.uint64))

@@ -179,6 +179,12 @@ def test_rvq_gpt2_config_full(fkv, orc):
     (32, 8, 33, 129, 1, 128), (128, 3, 256, 300, 4, 268), (48, 2, 64, 200, 0, 200),
     (256, 2, 256, 100, 0, 100), (64, 4, 256, 1024, 4, 992), (96, 1, 1, 50, 0, 50),
     (64, 2, 64, 1, 0, 1),
+    # every head dimension the kernel is built for, padded books (K not a multiple of 64),
+    # deep residuals (hi/lo carried residuals) and single-buffer books (d = 256, S > 2)
+    (80, 2, 65, 90, 0, 90), (112, 3, 129, 70, 2, 70), (144, 2, 200, 64, 0, 64),
+    (160, 5, 96, 60, 3, 60), (176, 2, 255, 40, 0, 40), (192, 3, 256, 50, 0, 50),
+    (208, 2, 130, 33, 0, 33), (224, 4, 64, 45, 5, 45), (240, 2, 100, 40, 0, 40),
+    (256, 3, 256, 70, 2, 70), (128, 8, 256, 80, 0, 80), (32, 6, 17, 300, 10, 290),
 ])
 def test_rvq_shapes(fkv, orc, d, S, K, T, t0, t1):
     rng = np.random.default_rng(d * 7 + S * 13 + K)
