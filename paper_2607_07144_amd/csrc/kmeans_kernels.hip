@@ -1,16 +1,19 @@
 // kmeans_kernels.hip -- one Lloyd update of a residual stage of per-head
 // codebooks (Sec. 3 "Setup": codebooks are trained by k-means), for gfx950.
 //
-// The assignment step is fkv_rvq_assign.  Accumulate: one lane per 8
-// dimensions of one archived token forms the stage input r = x - (codewords of
-// the earlier stages) exactly in fp64 and adds it, as an integer in units of
-// 2^-24 (every binary16 value is a multiple of 2^-24), to its cluster's sum with
-// 64-bit atomics -- integer addition, so the sums do not depend on the order
-// of the atomics.  Finalize: mean = sum / count * 2^-24 in fp64, rounded once to
+// The assignment step is fkv_rvq_assign.  Accumulate: one block per book and
+// 64-dimension slice; one lane per 8 dimensions of a member token forms the
+// stage input r = x - (codewords of the earlier stages) exactly in fp64 and
+// adds it, as an integer in units of 2^-24 (every binary16 value is a multiple
+// of 2^-24), to its cluster's sum with 64-bit LDS atomics -- integer addition,
+// so the sums do not depend on the order of the atomics.  Finalize: mean = sum / count * 2^-24 in fp64, rounded once to
 // binary16; an empty cluster keeps its centroid.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
+
+#include <algorithm>
+#include <mutex>
 
 #include "fkv.h"
 #include "fkv_hip_common.h"
@@ -23,37 +26,59 @@ namespace {
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 constexpr int kThreads = 256;
 
+// One block per (book, 64-dimension slice): the block owns that slice of the
+// book's cluster sums, accumulates every member token of every stream of the
+// book into LDS (64-bit LDS atomics), then adds the slice to the global sums
+// with plain read-modify-writes (no other block touches it in this launch).
+constexpr int kSlice = 64;
+
 __global__ __launch_bounds__(kThreads) void kmeans_accumulate_kernel(
     const _Float16* __restrict__ x, const _Float16* __restrict__ books, const int32_t* __restrict__ stream_book,
     const uint8_t* __restrict__ symbols, unsigned long long* __restrict__ sums, uint32_t* __restrict__ counts,
-    int64_t T, int64_t t_begin, int64_t Ta, int d, int S, int K, int n_books, int stage, int64_t n_tasks)
+    int64_t n_streams, int64_t T, int64_t t_begin, int64_t Ta, int d, int S, int K, int stage)
 {
-    const int nch = d / 8;
-    for (int64_t task = (int64_t)blockIdx.x * kThreads + threadIdx.x; task < n_tasks;
-         task += (int64_t)gridDim.x * kThreads) {
-        const int64_t tok = task / nch;   // stream * Ta + t
-        const int ch = (int)(task - tok * nch);
-        const int64_t s = tok / Ta, t = tok - s * Ta;
-        const int b = stream_book[s];
-        if (b < 0 || b >= n_books) continue;
-        const uint8_t* sym = symbols + tok * S;
-        bool bad = false;
-        for (int st = 0; st <= stage; ++st) bad = bad || sym[st] >= K;
-        if (bad) continue;   // a symbol outside the book: the token is skipped
-        const half8 xv = *(const half8*)(x + (s * T + t_begin + t) * d + ch * 8);
-        double r[8];
+    extern __shared__ __align__(16) uint8_t lds[];
+    const int n_slices = (d + kSlice - 1) / kSlice;
+    const int b = blockIdx.x / n_slices, slice = blockIdx.x - b * n_slices;
+    const int e0 = slice * kSlice, dc = min(kSlice, d - e0);   // this block's dimensions [e0, e0 + dc)
+    const int nch = dc / 8;
+    unsigned long long* ls = (unsigned long long*)lds;           // [K][dc]
+    uint32_t* lc = (uint32_t*)(ls + (size_t)K * dc);             // [K]
+    for (int i = threadIdx.x; i < K * dc; i += kThreads) ls[i] = 0;
+    for (int i = threadIdx.x; i < K; i += kThreads) lc[i] = 0;
+    __syncthreads();
+    for (int64_t s = 0; s < n_streams; ++s) {
+        if (stream_book[s] != b) continue;   // uniform across the block
+        for (int64_t task = threadIdx.x; task < Ta * nch; task += kThreads) {
+            const int64_t t = task / nch;
+            const int ch = (int)(task - t * nch);
+            const uint8_t* sym = symbols + (s * Ta + t) * S;
+            bool bad = false;
+            for (int st = 0; st <= stage; ++st) bad = bad || sym[st] >= K;
+            if (bad) continue;   // a symbol outside the book: the token is skipped
+            const half8 xv = *(const half8*)(x + (s * T + t_begin + t) * d + e0 + ch * 8);
+            double r[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) r[e] = (double)xv[e];
-        for (int st = 0; st < stage; ++st) {
-            const half8 c = *(const half8*)(books + (((int64_t)b * S + st) * K + sym[st]) * d + ch * 8);
+            for (int e = 0; e < 8; ++e) r[e] = (double)xv[e];
+            for (int st = 0; st < stage; ++st) {
+                const half8 c = *(const half8*)(books + (((int64_t)b * S + st) * K + sym[st]) * d + e0 + ch * 8);
 #pragma unroll
-            for (int e = 0; e < 8; ++e) r[e] = r[e] - (double)c[e];
+                for (int e = 0; e < 8; ++e) r[e] = r[e] - (double)c[e];
+            }
+            unsigned long long* dst = ls + (size_t)sym[stage] * dc + ch * 8;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) atomicAdd(dst + e, (unsigned long long)(long long)ldexp(r[e], 24));
+            if (ch == 0 && slice == 0) atomicAdd(lc + sym[stage], 1u);
         }
-        unsigned long long* dst = sums + ((int64_t)b * K + sym[stage]) * d + ch * 8;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) atomicAdd(dst + e, (unsigned long long)(long long)ldexp(r[e], 24));
-        if (ch == 0) atomicAdd(counts + (int64_t)b * K + sym[stage], 1u);
     }
+    __syncthreads();
+    for (int i = threadIdx.x; i < K * dc; i += kThreads) {
+        const int j = i / dc, e = i - j * dc;
+        if (ls[i]) sums[((int64_t)b * K + j) * d + e0 + e] += ls[i];
+    }
+    if (slice == 0)
+        for (int j = threadIdx.x; j < K; j += kThreads)
+            if (lc[j]) counts[(int64_t)b * K + j] += lc[j];
 }
 
 __global__ __launch_bounds__(kThreads) void kmeans_finalize_kernel(
@@ -98,10 +123,17 @@ extern "C" int fkv_kmeans_accumulate(const fkv_rvq_desc* desc, const uint16_t* x
     if (!aligned(x_f16, 16) || !aligned(books_f16, 16) || !aligned(sums, 8) || !aligned(counts, 4) ||
         !aligned(stream_book, 4))
         return FKV_ERR_INVALID_ARG;
-    const int64_t n_tasks = D.n_streams * Ta * (D.d / 8);
-    hipLaunchKernelGGL(kmeans_accumulate_kernel, dim3((unsigned)grid_for(n_tasks)), dim3(kThreads), 0,
+    const int n_slices = (D.d + kSlice - 1) / kSlice;
+    const size_t shm = (size_t)D.K * std::min(kSlice, (int)D.d) * 8 + (size_t)D.K * 4;
+    static std::once_flag once;
+    std::call_once(once, [] {
+        (void)hipFuncSetAttribute((const void*)kmeans_accumulate_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                  256 * kSlice * 8 + 256 * 4);
+    });
+    (void)hipGetLastError();
+    hipLaunchKernelGGL(kmeans_accumulate_kernel, dim3((unsigned)(D.n_books * n_slices)), dim3(kThreads), shm,
                        (hipStream_t)stream, (const _Float16*)x_f16, (const _Float16*)books_f16, stream_book, symbols,
-                       (unsigned long long*)sums, counts, D.T, D.t_begin, Ta, D.d, D.S, D.K, D.n_books, stage, n_tasks);
+                       (unsigned long long*)sums, counts, D.n_streams, D.T, D.t_begin, Ta, D.d, D.S, D.K, stage);
     return launch_status();
 }
 
