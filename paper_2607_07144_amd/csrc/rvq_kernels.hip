@@ -652,7 +652,9 @@ extern "C" int fkv_rvq_assign_encode(const fkv_rvq_desc* desc, const uint16_t* x
                                      uint8_t* symbols, double* points, float* residual, uint32_t* n_bad_streams,
                                      void* stream)
 {
-    if (!c || c->N < 3 || c->N > 256 || c->L < 1 || c->L > 64 || !(c->r > 0.0 && c->r < 1.0)) return FKV_ERR_INVALID_ARG;
+    if (!c || c->N < 3 || c->N > 256 || c->L < 1 || c->L > 64 || !(c->r > 0.0 && c->r < 1.0) ||
+        !(c->r_max > 0.0 && c->r <= c->r_max * (1.0 + 1e-12)))
+        return FKV_ERR_INVALID_ARG;
     if (!dev_table || !points || !aligned(dev_table, 16) || !aligned(points, 16)) return FKV_ERR_INVALID_ARG;
     const EncArgs enc = {(double2*)points, (const double2*)((const uint8_t*)dev_table + table_off_V(c->N)), c->r,
                          c->N, c->L};

@@ -194,3 +194,57 @@ def test_invalid_arguments_rehydrate_and_append(F):
     assert ap(sym=None) == E and ap(pts=None) == E and ap(pts=odd) == E
     assert ap(codec=F.fkv_codec(16, 0, 0.1, 0.2)) == E
     assert ap(m=0, sym=None, pts=None) == 0 and ap(ns=0, sym=None, pts=None) == 0
+
+
+def test_invalid_arguments_retrieval_kmeans_fused(F):
+    lib = F.lib
+    E = F.FKV_ERR_INVALID_ARG
+    c = F.fkv_codec()
+    assert lib.fkv_codec_init(16, 0.98, 0, ctypes.byref(c)) == 0
+    P = ctypes.c_void_p
+    g, odd = P(0x10000), P(0x10001)
+    too_big = F.fkv_codec(16, c.L, c.r_max * 1.001, c.r_max)       # r beyond the open-set bound
+
+    def tr(W=16, ns=2, n=100, sym=g, out=g, codec=c):
+        return lib.fkv_trajectory(ctypes.byref(codec), g, sym, ns, n, W, out, None)
+
+    assert tr(W=0) == E and tr(W=65) == E and tr(ns=-1) == E and tr(n=-1) == E
+    assert tr(sym=None) == E and tr(out=None) == E and tr(out=P(0x10008)) == E and tr(sym=odd) == E
+    assert tr(codec=too_big) == E
+    assert tr(ns=0, sym=None, out=None) == 0 and tr(n=0, sym=None, out=None) == 0
+
+    def ss(ell=3, verify=1, q=g, hits=g, mh=10, nh=g, nc=None, tj=g, ns=2, n=100, codec=c):
+        return lib.fkv_suffix_search(ctypes.byref(codec), g, tj, ns, n, q, ell, verify, hits, mh, nh, nc, None)
+
+    assert ss(ell=0) == E and ss(ell=17) == E        # 1 <= ell <= L (L = 16 here)
+    assert ss(verify=2) == E and ss(q=None) == E and ss(nh=None) == E and ss(nh=odd) == E
+    assert ss(hits=None) == E and ss(hits=P(0x10004)) == E and ss(mh=-1) == E
+    assert ss(tj=None) == E and ss(tj=P(0x10008)) == E and ss(codec=too_big) == E
+    assert ss(hits=None, mh=0, tj=None, ns=0) == 0
+
+    D = F.fkv_rvq_desc
+    good = D(4, 100, 4, 68, 64, 2, 256, 4)
+
+    def acc(desc=good, stage=0, x=g, b=g, sb=g, sym=g, sums=g, cnt=g):
+        return lib.fkv_kmeans_accumulate(ctypes.byref(desc) if desc is not None else None, x, b, sb, sym, stage,
+                                         sums, cnt, None)
+
+    assert acc(None) == E and acc(stage=2) == E and acc(stage=-1) == E
+    assert acc(D(4, 100, 4, 101, 64, 2, 256, 4)) == E and acc(D(4, 100, 4, 68, 64, 2, 257, 4)) == E
+    assert acc(x=None) == E and acc(sums=None) == E and acc(cnt=None) == E and acc(sym=None) == E
+
+    def fin(nb=4, S=2, K=256, d=64, stage=0, sums=g, cnt=g, b=g):
+        return lib.fkv_kmeans_finalize(nb, S, K, d, stage, sums, cnt, b, None)
+
+    assert fin(nb=0) == E and fin(S=9) == E and fin(K=0) == E and fin(K=257) == E
+    assert fin(d=12) == E and fin(d=264) == E and fin(stage=2) == E
+    assert fin(sums=None) == E and fin(sums=P(0x10004)) == E and fin(cnt=odd) == E and fin(b=odd) == E
+
+    def fused(desc=good, codec=c, tab=g, pts=g):
+        return lib.fkv_rvq_assign_encode(ctypes.byref(desc), g, g, g, ctypes.byref(codec), tab, g, pts, None,
+                                         None, None)
+
+    assert fused(codec=too_big) == E and fused(codec=F.fkv_codec(16, 0, 0.1, 0.2)) == E
+    assert fused(codec=F.fkv_codec(2, 6, 0.1, 0.2)) == E
+    assert fused(tab=None) == E and fused(pts=None) == E and fused(pts=P(0x10008)) == E
+    assert fused(D(4, 100, 4, 101, 64, 2, 256, 4)) == E
