@@ -148,9 +148,11 @@ __global__ __launch_bounds__(kBlock) void trajectory_kernel(const uint8_t* __res
     uint8_t* tile = lds + 256 * sizeof(double2);
     V[threadIdx.x] = (int)threadIdx.x < N ? ((const double2*)(gtab + table_off_V(N)))[threadIdx.x]
                                           : make_double2(NAN, NAN);
-    for (int64_t tl = blockIdx.x; tl < n_tiles; tl += gridDim.x) {
-        const int64_t s = tl / tiles_per_stream;
-        const int64_t k0 = (tl - s * tiles_per_stream) * kBlock;
+    TileWalk w;
+    w.init(blockIdx.x, gridDim.x, tiles_per_stream);
+    for (int64_t tl = blockIdx.x; tl < n_tiles; tl += gridDim.x, w.next()) {
+        const int64_t s = w.s;
+        const int64_t k0 = w.j * kBlock;
         const int64_t a0 = max((int64_t)0, k0 - W + 1);
         const int64_t k1 = min(n_sym, k0 + kBlock);
         const int64_t g0 = s * n_sym + a0, g1 = s * n_sym + k1;

@@ -54,10 +54,22 @@ __device__ inline Tables stage_tables(const uint8_t* __restrict__ gtab, int N, u
     uint4* l = (uint4*)lds;
     const int iW = (int)(table_off_W(N) / 16), iWr = (int)(table_off_Wr(N) / 16);
     const int n16 = (int)(table_bytes(N) / 16);
-    for (int i = threadIdx.x; i < n16; i += blockDim.x) {
-        if (i < iW && !needV) continue;
-        if (i >= iW && i < iWr && !needW) continue;
-        l[i] = g[i];
+    // four loads in flight per thread before any is stored (indices clamped
+    // into the table; only the wanted ones are stored)
+    const int bd = blockDim.x;
+    for (int i0 = threadIdx.x; i0 < n16; i0 += 4 * bd) {
+        const int i1 = i0 + bd, i2 = i0 + 2 * bd, i3 = i0 + 3 * bd;
+        const uint4 v0 = g[i0];
+        const uint4 v1 = g[min(i1, n16 - 1)];
+        const uint4 v2 = g[min(i2, n16 - 1)];
+        const uint4 v3 = g[min(i3, n16 - 1)];
+        auto put = [&](int i, const uint4& v) {
+            if (i < n16 && (needV || i >= iW) && (needW || i < iW || i >= iWr)) l[i] = v;
+        };
+        put(i0, v0);
+        put(i1, v1);
+        put(i2, v2);
+        put(i3, v3);
     }
     return t;
 }
@@ -160,6 +172,33 @@ __device__ inline int lookup_token(const double2* __restrict__ pts, const Tables
     *got = g;
     return status;
 }
+
+// The tiles tl = blockIdx.x + i gridDim.x of a persistent block as (stream,
+// tile within the stream), advanced with additions only: a 64-bit division
+// per tile is emulated on the scalar unit and costs more than the tile's own
+// scalar work.
+struct TileWalk {
+    int64_t s, j;           // stream, tile within the stream
+    int64_t ds, dj, tps;    // the grid stride as (streams, tiles); tiles per stream
+
+    __device__ void init(int64_t tl, int64_t stride, int64_t tiles_per_stream)
+    {
+        tps = tiles_per_stream;
+        s = tl / tps;
+        j = tl - s * tps;
+        ds = stride / tps;
+        dj = stride - ds * tps;
+    }
+    __device__ void next()
+    {
+        s += ds;
+        j += dj;
+        if (j >= tps) {
+            j -= tps;
+            ++s;
+        }
+    }
+};
 
 int64_t blocks_for(int64_t n_tiles)
 {

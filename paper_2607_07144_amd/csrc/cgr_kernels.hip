@@ -7,11 +7,12 @@
 // (sector) that holds the point and inverts the map, p <- (p - (1-r)V(c)) / r,
 // walking back to the anchor.
 //
-// Layout: one span per lane, 256 spans per block tile, tiles of one stream are
-// contiguous in both the symbol bytes and the 16-byte points, so every global
-// access of a tile is a coalesced stream; symbol bytes are staged through LDS.
-// The per-alphabet tables (vertices, cell centres, sector look-up) live in LDS
-// for the whole persistent block.
+// Layout: one span per lane; the spans of a tile are contiguous in both the
+// symbol bytes and the 16-byte points, so every global access of a tile is a
+// coalesced stream.  Encode reads each span's bytes straight from the aligned
+// dwords that cover it (spans of up to 16 symbols); longer spans, and decode's
+// output, go through LDS.  The per-alphabet tables (vertices, cell centres,
+// sector look-up) live in LDS for the whole persistent block.
 //
 // Floating point: the encode recurrence must be bit-reproducible, so this file
 // is compiled without FP contraction, and fused multiply-adds appear only where
@@ -24,7 +25,8 @@ namespace {
 
 // ------------------------------------------------------------------ encode --
 
-__global__ __launch_bounds__(kBlock) void cgr_encode_kernel(
+// Span encode through an LDS tile of 256 spans (spans longer than 16 symbols).
+__global__ __launch_bounds__(kBlock, 8) void cgr_encode_tiles_kernel(
     const uint8_t* __restrict__ sym, double2* __restrict__ pts, const uint8_t* __restrict__ gtab,
     CodecArgs cd, int64_t n_sym, int64_t n_spans, int64_t tiles_per_stream, int64_t n_tiles)
 {
@@ -40,9 +42,11 @@ __global__ __launch_bounds__(kBlock) void cgr_encode_kernel(
     const double2 vreg = (int)threadIdx.x < N ? ((const double2*)(gtab + table_off_V(N)))[threadIdx.x]
                                               : make_double2(NAN, NAN);
     bool staged = false;
-    for (int64_t tl = blockIdx.x; tl < n_tiles; tl += gridDim.x) {
-        const int64_t s = tl / tiles_per_stream;
-        const int64_t j0 = (tl - s * tiles_per_stream) * kBlock;
+    TileWalk cur;
+    cur.init(blockIdx.x, gridDim.x, tiles_per_stream);
+    for (int64_t tl = blockIdx.x; tl < n_tiles; tl += gridDim.x, cur.next()) {
+        const int64_t s = cur.s;
+        const int64_t j0 = cur.j * kBlock;
         const int64_t nsp = min((int64_t)kBlock, n_spans - j0);
         const int64_t g0 = s * n_sym + j0 * L;
         const int64_t g1 = s * n_sym + min(n_sym, (j0 + nsp) * L);
@@ -64,39 +68,101 @@ __global__ __launch_bounds__(kBlock) void cgr_encode_kernel(
     }
 }
 
+// Span encode for spans of up to 16 symbols, with no LDS staging: a wave
+// takes 64 consecutive spans of one stream (a wave tile), each lane loads the
+// two to five aligned dwords that cover its span, extracts the symbols and
+// walks them from the anchor.  Wave tiles are walked without division.
+__global__ __launch_bounds__(kBlock, 8) void cgr_encode_kernel(
+    const uint8_t* __restrict__ sym, double2* __restrict__ pts, const uint8_t* __restrict__ gtab,
+    CodecArgs cd, int64_t n_sym, int64_t n_spans, int64_t wtiles_per_stream, int64_t n_wtiles, int64_t total_bytes)
+{
+    __shared__ double2 V[256];   // entries >= N are NaN: a symbol outside the alphabet gives a NaN point
+    const int N = cd.N, L = cd.L;
+    static_assert(kBlock == 256, "one vertex entry per thread");
+    V[threadIdx.x] = (int)threadIdx.x < N ? ((const double2*)(gtab + table_off_V(N)))[threadIdx.x]
+                                          : make_double2(NAN, NAN);
+    __syncthreads();
+    const int lane = threadIdx.x & 63;
+    const int64_t wave = (int64_t)blockIdx.x * (kBlock / 64) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t n_waves = (int64_t)gridDim.x * (kBlock / 64);
+    const uint32_t* s32 = (const uint32_t*)sym;
+    const int64_t n_dw = total_bytes >> 2;   // whole dwords of the symbol array
+    TileWalk w;
+    w.init(wave, n_waves, wtiles_per_stream);
+    for (int64_t t = wave; t < n_wtiles; t += n_waves, w.next()) {
+        const int64_t j = w.j * 64 + lane;
+        if (j >= n_spans) continue;
+        const int64_t a = w.s * n_sym + j * L;
+        const int len = (int)min((int64_t)L, n_sym - j * L);
+        const int off = (int)(a & 3);
+        const int64_t d0 = a >> 2;
+        uint32_t dw[5];
+#pragma unroll
+        for (int q = 0; q < 5; ++q) {
+            const int64_t d = d0 + q;
+            dw[q] = 0;
+            if (q * 4 < off + len) {
+                if (d < n_dw) {
+                    dw[q] = s32[d];
+                } else {   // the array's last, partial dword, byte by byte
+                    for (int b = 0; b < 4 && d * 4 + b < total_bytes; ++b) dw[q] |= (uint32_t)sym[d * 4 + b] << (8 * b);
+                }
+            }
+        }
+        uint32_t e[4];   // symbols 4c..4c+3 of the span
+#pragma unroll
+        for (int c = 0; c < 4; ++c) e[c] = __builtin_amdgcn_alignbyte(dw[c + 1], dw[c], off);
+        double px = 0.0, py = 0.0;
+#pragma unroll
+        for (int k = 0; k < 16; ++k)
+            if (k < len) encode_step(px, py, V[(e[k >> 2] >> (8 * (k & 3))) & 0xFF], cd.r);
+        pts[w.s * n_spans + j] = make_double2(px, py);
+    }
+}
+
 // ------------------------------------------------------------------ decode --
 
+// Bulk decode with no block barrier after the table staging: a wave decodes
+// 64 consecutive spans of one stream (a wave tile) into its own LDS staging
+// area and writes them back as aligned dwords (bytes at either end); the
+// point of its next wave tile is loaded while the current one decodes.
 template <bool EXACT, bool VERIFY>
-__global__ __launch_bounds__(kBlock) void cgr_decode_kernel(
+__global__ __launch_bounds__(kBlock, 8) void cgr_decode_kernel(
     const double2* __restrict__ pts, uint8_t* __restrict__ sym, uint8_t* __restrict__ span_ok,
     uint32_t* __restrict__ n_failed, const uint8_t* __restrict__ gtab, CodecArgs cd, int64_t n_sym,
-    int64_t n_spans, int64_t tiles_per_stream, int64_t n_tiles)
+    int64_t n_spans, int64_t wtiles_per_stream, int64_t n_wtiles, int stage_bytes)
 {
     extern __shared__ __align__(16) uint8_t lds[];
     const int N = cd.N, L = cd.L;
-    // The first tile's point is loaded before the tables are staged, so the
-    // two memory latencies overlap.
-    double2 P0 = make_double2(0.0, 0.0);
-    if ((int64_t)blockIdx.x < n_tiles) {
-        const int64_t s = (int64_t)blockIdx.x / tiles_per_stream;
-        const int64_t j0 = ((int64_t)blockIdx.x - s * tiles_per_stream) * kBlock;
-        if ((int64_t)threadIdx.x < min((int64_t)kBlock, n_spans - j0)) P0 = pts[s * n_spans + j0 + threadIdx.x];
-    }
+    const int lane = threadIdx.x & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t wave = (int64_t)blockIdx.x * (kBlock / 64) + wv;
+    const int64_t n_waves = (int64_t)gridDim.x * (kBlock / 64);
+    TileWalk cur, nxt;
+    cur.init(wave, n_waves, wtiles_per_stream);
+    nxt = cur;
+    nxt.next();
+    // the first wave tile's point is loaded before the tables are staged, so
+    // the two memory latencies overlap
+    double2 Pcur = make_double2(0.0, 0.0);
+    if (wave < n_wtiles && cur.j * 64 + lane < n_spans) Pcur = pts[cur.s * n_spans + cur.j * 64 + lane];
     Tables t = stage_tables(gtab, N, lds, VERIFY, EXACT);
-    uint8_t* tile = lds + table_bytes(N);
-    for (int64_t tl = blockIdx.x; tl < n_tiles; tl += gridDim.x) {
-        const int64_t s = tl / tiles_per_stream;
-        const int64_t j0 = (tl - s * tiles_per_stream) * kBlock;
-        const int64_t nsp = min((int64_t)kBlock, n_spans - j0);
+    uint8_t* stage = lds + table_bytes(N) + (size_t)wv * stage_bytes;
+    __syncthreads();   // tables staged
+    for (int64_t tw = wave; tw < n_wtiles; tw += n_waves, cur.next(), nxt.next()) {
+        const int64_t s = cur.s;
+        const int64_t j0 = cur.j * 64;
+        const int64_t nsp = min((int64_t)64, n_spans - j0);
         const int64_t g0 = s * n_sym + j0 * L;
         const int64_t g1 = s * n_sym + min(n_sym, (j0 + nsp) * L);
-        __syncthreads();  // tables staged / previous tile flushed
+        double2 Pnext = make_double2(0.0, 0.0);
+        if (tw + n_waves < n_wtiles && nxt.j * 64 + lane < n_spans) Pnext = pts[nxt.s * n_spans + nxt.j * 64 + lane];
         bool failed = false;
-        if (threadIdx.x < nsp) {
-            const int64_t a = (j0 + threadIdx.x) * L;
+        if (lane < nsp) {
+            const int64_t a = (j0 + lane) * L;
             const int len = (int)min((int64_t)L, n_sym - a);
-            uint8_t* my = tile + (g0 & 3) + threadIdx.x * L;
-            const double2 P = tl == (int64_t)blockIdx.x ? P0 : pts[s * n_spans + j0 + threadIdx.x];
+            uint8_t* my = stage + (g0 & 3) + lane * L;
+            const double2 P = Pcur;
             double qx = P.x, qy = P.y;
             for (int k = len - 1; k >= 0; --k) {
                 const int c = sector_of<EXACT>(qx, qy, t, N);
@@ -110,12 +176,15 @@ __global__ __launch_bounds__(kBlock) void cgr_decode_kernel(
                 ok = ok && (__double_as_longlong(px) == __double_as_longlong(P.x)) &&
                      (__double_as_longlong(py) == __double_as_longlong(P.y));
             }
-            if (span_ok) span_ok[s * n_spans + j0 + threadIdx.x] = ok ? 1 : 0;
+            if (span_ok) span_ok[s * n_spans + j0 + lane] = ok ? 1 : 0;
             failed = !ok;
         }
         count_flags(failed, n_failed);
-        __syncthreads();
-        lds_to_bytes(tile, g0, g1, sym);
+        // the wave's LDS writes above precede its reads below (a wave's LDS
+        // operations are performed in order)
+        __builtin_amdgcn_wave_barrier();
+        lds_to_bytes_wave(stage, g0, g1, sym, lane);
+        Pcur = Pnext;
     }
 }
 
@@ -176,10 +245,19 @@ extern "C" int fkv_cgr_encode_spans(const fkv_codec* c, const void* dev_table, c
     if (!symbols || !points || !aligned(dev_table, 16) || !aligned(points, 16) || !aligned(symbols, 4))
         return FKV_ERR_INVALID_ARG;
     const int64_t n_spans = (n_sym + c->L - 1) / c->L;
+    if (c->L <= 16) {
+        const int64_t wtps = (n_spans + 63) / 64;
+        const int64_t n_wtiles = wtps * n_streams;
+        const int64_t nb = min((int64_t)kMaxBlocks, (n_wtiles + kBlock / 64 - 1) / (kBlock / 64));
+        hipLaunchKernelGGL(cgr_encode_kernel, dim3((unsigned)nb), dim3(kBlock), 0, (hipStream_t)stream, symbols,
+                           (double2*)points, (const uint8_t*)dev_table, codec_args(c), n_sym, n_spans, wtps,
+                           n_wtiles, n_streams * n_sym);
+        return launch_status();
+    }
     const int64_t tps = (n_spans + kBlock - 1) / kBlock;
     const int64_t n_tiles = tps * n_streams;
     const size_t shm = 256 * 16 + (size_t)kBlock * c->L + 16;
-    hipLaunchKernelGGL(cgr_encode_kernel, dim3((unsigned)blocks_for(n_tiles)), dim3(kBlock), shm,
+    hipLaunchKernelGGL(cgr_encode_tiles_kernel, dim3((unsigned)blocks_for(n_tiles)), dim3(kBlock), shm,
                        (hipStream_t)stream, symbols, (double2*)points, (const uint8_t*)dev_table,
                        codec_args(c), n_sym, n_spans, tps, n_tiles);
     return launch_status();
@@ -196,27 +274,28 @@ extern "C" int fkv_cgr_decode_spans(const fkv_codec* c, const void* dev_table, c
         return FKV_ERR_INVALID_ARG;
     if (n_failed && !aligned(n_failed, 4)) return FKV_ERR_INVALID_ARG;
     const int64_t n_spans = (n_sym + c->L - 1) / c->L;
-    const int64_t tps = (n_spans + kBlock - 1) / kBlock;
-    const int64_t n_tiles = tps * n_streams;
-    const size_t shm = table_bytes(c->N) + (size_t)kBlock * c->L + 16;
+    const int64_t wtps = (n_spans + 63) / 64;
+    const int64_t n_wtiles = wtps * n_streams;
+    const int stage_bytes = (64 * c->L + 4 + 15) / 16 * 16;   // one wave tile's symbols, dword-shifted
+    const size_t shm = table_bytes(c->N) + (size_t)(kBlock / 64) * stage_bytes;
     const bool exact = needs_exact_sectors(c);
-    const dim3 grid((unsigned)blocks_for(n_tiles)), block(kBlock);
+    const dim3 grid((unsigned)min((int64_t)kMaxBlocks, (n_wtiles + kBlock / 64 - 1) / (kBlock / 64))), block(kBlock);
     const hipStream_t st = (hipStream_t)stream;
     const double2* P = (const double2*)points;
     const uint8_t* tb = (const uint8_t*)dev_table;
     const CodecArgs a = codec_args(c);
     if (exact && verify)
         hipLaunchKernelGGL((cgr_decode_kernel<true, true>), grid, block, shm, st, P, symbols, span_ok,
-                           n_failed, tb, a, n_sym, n_spans, tps, n_tiles);
+                           n_failed, tb, a, n_sym, n_spans, wtps, n_wtiles, stage_bytes);
     else if (exact)
         hipLaunchKernelGGL((cgr_decode_kernel<true, false>), grid, block, shm, st, P, symbols, span_ok,
-                           n_failed, tb, a, n_sym, n_spans, tps, n_tiles);
+                           n_failed, tb, a, n_sym, n_spans, wtps, n_wtiles, stage_bytes);
     else if (verify)
         hipLaunchKernelGGL((cgr_decode_kernel<false, true>), grid, block, shm, st, P, symbols, span_ok,
-                           n_failed, tb, a, n_sym, n_spans, tps, n_tiles);
+                           n_failed, tb, a, n_sym, n_spans, wtps, n_wtiles, stage_bytes);
     else
         hipLaunchKernelGGL((cgr_decode_kernel<false, false>), grid, block, shm, st, P, symbols, span_ok,
-                           n_failed, tb, a, n_sym, n_spans, tps, n_tiles);
+                           n_failed, tb, a, n_sym, n_spans, wtps, n_wtiles, stage_bytes);
     return launch_status();
 }
 

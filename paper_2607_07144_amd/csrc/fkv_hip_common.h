@@ -60,6 +60,26 @@ __device__ inline void lds_to_bytes(const uint8_t* lds, int64_t g0, int64_t g1,
     if (tid < g1 - a1) dst[a1 + tid] = lds[a1 + tid - base];
 }
 
+// One wave's counterpart of lds_to_bytes: its 64 lanes write LDS bytes back to
+// global [g0, g1), whole aligned dwords as dwords and the partial dwords at
+// either end byte by byte (so nothing outside [g0, g1) is written).
+__device__ inline void lds_to_bytes_wave(const uint8_t* lds, int64_t g0, int64_t g1, uint8_t* __restrict__ dst,
+                                         int lane)
+{
+    const int64_t base = g0 & ~(int64_t)3;
+    const int64_t a0 = (g0 + 3) & ~(int64_t)3;
+    const int64_t a1 = g1 & ~(int64_t)3;
+    if (a0 >= a1) {
+        for (int64_t g = g0 + lane; g < g1; g += 64) dst[g] = lds[g - base];
+        return;
+    }
+    uint32_t* d32 = (uint32_t*)dst;
+    const uint32_t* l32 = (const uint32_t*)(lds + (a0 - base));
+    for (int64_t w = (a0 >> 2) + lane; w < (a1 >> 2); w += 64) d32[w] = l32[w - (a0 >> 2)];
+    if (lane < a0 - g0) dst[g0 + lane] = lds[g0 + lane - base];
+    if (lane < g1 - a1) dst[a1 + lane] = lds[a1 + lane - base];
+}
+
 // Correctly rounded binary64 -> binary16 (round to nearest, ties to even): the
 // conversion to binary32 is made round-to-odd (truncate, then set the last
 // bit when inexact), which carries enough information for the final
