@@ -36,8 +36,8 @@ __global__ __launch_bounds__(kBlock) void rehydrate_kernel(
     Tables t = stage_tables(gtab, N, lds, false, EXACT);
     // After the tables: each query of the current batch's book id (-1: no
     // output) and its packed symbols.
-    int32_t* qbook = (int32_t*)(lds + table_bytes(N));
-    uint64_t* qsym = (uint64_t*)(lds + table_bytes(N) + kBlock * sizeof(int32_t));
+    int32_t* qbook = (int32_t*)(lds + staged_table_bytes(N, false, EXACT));
+    uint64_t* qsym = (uint64_t*)(lds + staged_table_bytes(N, false, EXACT) + kBlock * sizeof(int32_t));
     __syncthreads();
     const int64_t n_tok = n_sym / S;
     const int nch = d / 8;   // 16-byte chunks per output row
@@ -179,7 +179,7 @@ __global__ __launch_bounds__(kBlock) void suffix_search_kernel(
     extern __shared__ __align__(16) uint8_t lds[];
     const int N = cd.N;
     Tables t = stage_tables(gtab, N, lds, true, EXACT);
-    uint8_t* qs = lds + table_bytes(N);
+    uint8_t* qs = lds + staged_table_bytes(N, true, EXACT);
     if ((int)threadIdx.x < ell) qs[threadIdx.x] = query[threadIdx.x];
     __syncthreads();
     // the query's point from the origin and the threshold, as in the index; a
@@ -212,7 +212,7 @@ __global__ __launch_bounds__(kBlock) void suffix_search_kernel(
                 if (VERIFY && cand) {
                     double x = p.x, y = p.y;
                     for (int j = ell - 1; j >= 0; --j) {
-                        const int c = sector_of<EXACT>(x, y, t, N);
+                        const int c = sector_of<EXACT>(x, y, t, cd);
                         if (c != qs[j]) {
                             hit = false;
                             break;
@@ -262,7 +262,8 @@ extern "C" int fkv_rehydrate(const fkv_codec* c, const void* dev_table, const do
     if ((stream_book && !aligned(stream_book, 4)) || (n_failed && !aligned(n_failed, 4)))
         return FKV_ERR_INVALID_ARG;
     const int64_t n_spans = (n_sym + c->L - 1) / c->L;
-    const size_t shm = table_bytes(c->N) + (size_t)kBlock * (sizeof(int32_t) + sizeof(uint64_t));
+    const size_t shm =
+        staged_table_bytes(c->N, false, needs_exact_sectors(c)) + (size_t)kBlock * (sizeof(int32_t) + sizeof(uint64_t));
     const int64_t nb = blocks_for((n_q + kBlock - 1) / kBlock);
     const hipStream_t st = (hipStream_t)stream;
     if (needs_exact_sectors(c))
@@ -321,14 +322,14 @@ extern "C" int fkv_suffix_search(const fkv_codec* c, const void* dev_table, cons
         return FKV_ERR_INVALID_ARG;
     if (n_streams == 0 || n_sym == 0) return FKV_OK;
     if (!traj || !aligned(traj, 16)) return FKV_ERR_INVALID_ARG;
-    const size_t shm = table_bytes(c->N) + 64;
+    const bool exact = needs_exact_sectors(c);
+    const size_t shm = staged_table_bytes(c->N, true, exact) + 64;
     const int64_t nb = blocks_for((n_streams * n_sym + kBlock - 1) / kBlock);
     const dim3 grid((unsigned)nb), block(kBlock);
     const hipStream_t st = (hipStream_t)stream;
     const double2* T = (const double2*)traj;
     const uint8_t* tb = (const uint8_t*)dev_table;
     const CodecArgs a = codec_args(c);
-    const bool exact = needs_exact_sectors(c);
     if (exact && verify)
         hipLaunchKernelGGL((suffix_search_kernel<true, true>), grid, block, shm, st, T, query, tb, a, n_streams,
                            n_sym, ell, hits, max_hits, n_hits, n_candidates);

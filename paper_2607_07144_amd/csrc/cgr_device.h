@@ -30,6 +30,7 @@ struct CodecArgs {
     int L;
     double r;
     double inv_r;
+    float lut_bias;   // 2 kLutPerUnit + lut_shift(N): bucket coordinate at R = 0
 };
 
 // LDS image of the device table, sized for the alphabet.
@@ -37,8 +38,15 @@ struct Tables {
     double2* V;
     double2* W;
     double2* Wr;
-    LutEntry* lut;
+    uint32_t* lut;
 };
+
+// Bytes of LDS the staged table occupies: Wr and the look-up table always,
+// then V and W when needed (sections keep their table offsets).
+__host__ __device__ constexpr size_t staged_table_bytes(int N, bool needV, bool needW)
+{
+    return needW ? table_bytes(N) : needV ? table_off_W(N) : table_fast_bytes(N);
+}
 
 // Copies the needed sections of the device table into LDS at the same
 // offsets (sections not needed are left unwritten).
@@ -49,13 +57,13 @@ __device__ inline Tables stage_tables(const uint8_t* __restrict__ gtab, int N, u
     t.V = (double2*)(lds + table_off_V(N));
     t.W = (double2*)(lds + table_off_W(N));
     t.Wr = (double2*)(lds + table_off_Wr(N));
-    t.lut = (LutEntry*)(lds + table_off_lut(N));
+    t.lut = (uint32_t*)(lds + table_off_lut(N));
     const uint4* g = (const uint4*)gtab;
     uint4* l = (uint4*)lds;
-    const int iW = (int)(table_off_W(N) / 16), iWr = (int)(table_off_Wr(N) / 16);
-    const int n16 = (int)(table_bytes(N) / 16);
+    const int iV = (int)(table_off_V(N) / 16), iW = (int)(table_off_W(N) / 16);
+    const int n16 = (int)(staged_table_bytes(N, needV, needW) / 16);
     // four loads in flight per thread before any is stored (indices clamped
-    // into the table; only the wanted ones are stored)
+    // into the staged range; only the wanted ones are stored)
     const int bd = blockDim.x;
     for (int i0 = threadIdx.x; i0 < n16; i0 += 4 * bd) {
         const int i1 = i0 + bd, i2 = i0 + 2 * bd, i3 = i0 + 3 * bd;
@@ -64,7 +72,7 @@ __device__ inline Tables stage_tables(const uint8_t* __restrict__ gtab, int N, u
         const uint4 v2 = g[min(i2, n16 - 1)];
         const uint4 v3 = g[min(i3, n16 - 1)];
         auto put = [&](int i, const uint4& v) {
-            if (i < n16 && (needV || i >= iW) && (needW || i < iW || i >= iWr)) l[i] = v;
+            if (i < n16 && (needV || i < iV || i >= iW)) l[i] = v;
         };
         put(i0, v0);
         put(i1, v1);
@@ -88,18 +96,19 @@ __device__ inline void encode_step(double& px, double& py, const double2 v, cons
 // Sector of a point from the pseudo-angle look-up table.  Exact for every
 // point at least kFastSectorMargin away from the sector lines (the fp32
 // pseudo-angle errs by < 1e-6 there); never leaves [0, N).
-__device__ inline int sector_fast(double qx, double qy, const LutEntry* __restrict__ lut)
+__device__ inline int sector_fast(double qx, double qy, const uint32_t* __restrict__ lut, float lut_bias)
 {
     const float fx = (float)qx;
     const float fy = (float)qy;
-    const float s = fabsf(fx) + fabsf(fy);
-    const float d = fy * __builtin_amdgcn_rcpf(s);
-    float P = fx >= 0.0f ? d : 2.0f - d;
-    P = fminf(fmaxf(P, -1.0f), 2.99999f);   // NaN (zero or non-finite input) -> -1
-    int idx = (int)((P + 1.0f) * (float)kLutPerUnit);
-    idx = min(idx, kLutBuckets - 1);
-    const LutEntry e = lut[idx];
-    return P >= e.thr ? e.hi : e.lo;
+    const float rs = __builtin_amdgcn_rcpf(fabsf(fx) + fabsf(fy));
+    // R = 1 - P = copysign(1 - y/(|x|+|y|), x), clamped into the table's
+    // range; zero or non-finite input gives NaN, which the clamp sends to -2
+    float R = __builtin_copysignf(__builtin_fmaf(-fy, rs, 1.0f), fx);
+    R = fminf(fmaxf(R, -1.99999f), 2.0f);
+    const float u = __builtin_fmaf(R, -(float)kLutPerUnit, lut_bias);   // in [0, 4 kLutPerUnit + 1)
+    const uint32_t e = lut[(int)u];
+    // lower-edge sector, plus one when the point lies past the bucket's boundary
+    return (int)(e & 0xFFu) + (__builtin_amdgcn_fractf(u) >= __uint_as_float(e) ? 1 : 0);
 }
 
 // Exact nearest cell centre, lowest index on exact ties (used when the margin
@@ -122,10 +131,10 @@ __device__ inline int sector_exact(double qx, double qy, const double2* __restri
 }
 
 template <bool EXACT>
-__device__ inline int sector_of(double qx, double qy, const Tables& t, int N)
+__device__ inline int sector_of(double qx, double qy, const Tables& t, const CodecArgs& cd)
 {
-    if (EXACT) return sector_exact(qx, qy, t.W, N);
-    return sector_fast(qx, qy, t.lut);
+    if (EXACT) return sector_exact(qx, qy, t.W, cd.N);
+    return sector_fast(qx, qy, t.lut, cd.lut_bias);
 }
 
 // Inverse map q <- (q - W(c)) / r, as q * (1/r) - W(c)/r with one rounding per
@@ -162,7 +171,7 @@ __device__ inline int lookup_token(const double2* __restrict__ pts, const Tables
         const double2 P = (has_p0 && j == j0) ? P0 : pts[s * n_spans + j];
         double qx = P.x, qy = P.y;
         for (int k = len - 1; k >= 0; --k) {
-            const int c = sector_of<EXACT>(qx, qy, t, cd.N);
+            const int c = sector_of<EXACT>(qx, qy, t, cd);
             const int64_t off = b + k - a;   // position within the token's S symbols
             if (off >= 0 && off < S) g |= (uint64_t)c << (8 * off);
             decode_step(qx, qy, t.Wr[c], cd.inv_r);
@@ -218,6 +227,7 @@ CodecArgs codec_args(const fkv_codec* c)
     a.L = c->L;
     a.r = c->r;
     a.inv_r = 1.0 / c->r;
+    a.lut_bias = (float)(2.0 * kLutPerUnit + lut_shift(c->N));
     return a;
 }
 

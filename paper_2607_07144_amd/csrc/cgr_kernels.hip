@@ -123,9 +123,28 @@ __global__ __launch_bounds__(kBlock, 8) void cgr_encode_kernel(
 // ------------------------------------------------------------------ decode --
 
 // Bulk decode with no block barrier after the table staging: a wave decodes
-// 64 consecutive spans of one stream (a wave tile) into its own LDS staging
-// area and writes them back as aligned dwords (bytes at either end); the
-// point of its next wave tile is loaded while the current one decodes.
+// 128 consecutive spans of one stream (a wave tile), two per lane walked as
+// independent chains so that the look-ups of one overlap the arithmetic of
+// the other, into its own LDS staging area, and writes them back as aligned
+// dwords (bytes at either end); the points of its next wave tile are loaded
+// while the current one decodes.
+constexpr int kDecodeSpl = 2;                  // spans per lane
+constexpr int kDecodeTile = 64 * kDecodeSpl;   // spans per wave tile
+
+template <bool EXACT, bool VERIFY>
+__device__ inline bool decode_finish(double qx, double qy, const double2 P, const uint8_t* my, int len,
+                                     const Tables& t, const CodecArgs& cd)
+{
+    bool ok = anchor_ok(qx, qy);
+    if (VERIFY) {
+        double px = 0.0, py = 0.0;
+        for (int k = 0; k < len; ++k) encode_step(px, py, t.V[my[k]], cd.r);
+        ok = ok && (__double_as_longlong(px) == __double_as_longlong(P.x)) &&
+             (__double_as_longlong(py) == __double_as_longlong(P.y));
+    }
+    return ok;
+}
+
 template <bool EXACT, bool VERIFY>
 __global__ __launch_bounds__(kBlock, 8) void cgr_decode_kernel(
     const double2* __restrict__ pts, uint8_t* __restrict__ sym, uint8_t* __restrict__ span_ok,
@@ -142,49 +161,77 @@ __global__ __launch_bounds__(kBlock, 8) void cgr_decode_kernel(
     cur.init(wave, n_waves, wtiles_per_stream);
     nxt = cur;
     nxt.next();
-    // the first wave tile's point is loaded before the tables are staged, so
-    // the two memory latencies overlap
-    double2 Pcur = make_double2(0.0, 0.0);
-    if (wave < n_wtiles && cur.j * 64 + lane < n_spans) Pcur = pts[cur.s * n_spans + cur.j * 64 + lane];
+    // the first wave tile's points are loaded before the tables are staged,
+    // so the two memory latencies overlap
+    const double2 zero = make_double2(0.0, 0.0);
+    double2 P0 = zero, P1 = zero;
+    if (wave < n_wtiles) {
+        const int64_t j = cur.j * kDecodeTile + lane;
+        if (j < n_spans) P0 = pts[cur.s * n_spans + j];
+        if (j + 64 < n_spans) P1 = pts[cur.s * n_spans + j + 64];
+    }
     Tables t = stage_tables(gtab, N, lds, VERIFY, EXACT);
-    uint8_t* stage = lds + table_bytes(N) + (size_t)wv * stage_bytes;
+    uint8_t* stage = lds + staged_table_bytes(N, VERIFY, EXACT) + (size_t)wv * stage_bytes;
     __syncthreads();   // tables staged
     for (int64_t tw = wave; tw < n_wtiles; tw += n_waves, cur.next(), nxt.next()) {
         const int64_t s = cur.s;
-        const int64_t j0 = cur.j * 64;
-        const int64_t nsp = min((int64_t)64, n_spans - j0);
+        const int64_t j0 = cur.j * kDecodeTile;
+        const int64_t nsp = min((int64_t)kDecodeTile, n_spans - j0);
         const int64_t g0 = s * n_sym + j0 * L;
         const int64_t g1 = s * n_sym + min(n_sym, (j0 + nsp) * L);
-        double2 Pnext = make_double2(0.0, 0.0);
-        if (tw + n_waves < n_wtiles && nxt.j * 64 + lane < n_spans) Pnext = pts[nxt.s * n_spans + nxt.j * 64 + lane];
-        bool failed = false;
-        if (lane < nsp) {
-            const int64_t a = (j0 + lane) * L;
-            const int len = (int)min((int64_t)L, n_sym - a);
-            uint8_t* my = stage + (g0 & 3) + lane * L;
-            const double2 P = Pcur;
-            double qx = P.x, qy = P.y;
-            for (int k = len - 1; k >= 0; --k) {
-                const int c = sector_of<EXACT>(qx, qy, t, N);
-                my[k] = (uint8_t)c;
-                decode_step(qx, qy, t.Wr[c], cd.inv_r);
-            }
-            bool ok = anchor_ok(qx, qy);
-            if (VERIFY) {
-                double px = 0.0, py = 0.0;
-                for (int k = 0; k < len; ++k) encode_step(px, py, t.V[my[k]], cd.r);
-                ok = ok && (__double_as_longlong(px) == __double_as_longlong(P.x)) &&
-                     (__double_as_longlong(py) == __double_as_longlong(P.y));
-            }
-            if (span_ok) span_ok[s * n_spans + j0 + lane] = ok ? 1 : 0;
-            failed = !ok;
+        double2 N0 = zero, N1 = zero;
+        if (tw + n_waves < n_wtiles) {
+            const int64_t j = nxt.j * kDecodeTile + lane;
+            if (j < n_spans) N0 = pts[nxt.s * n_spans + j];
+            if (j + 64 < n_spans) N1 = pts[nxt.s * n_spans + j + 64];
         }
-        count_flags(failed, n_failed);
+        uint8_t* my0 = stage + (g0 & 3) + lane * L;
+        uint8_t* my1 = my0 + 64 * L;
+        bool f0 = false, f1 = false;
+        if (nsp == kDecodeTile && (j0 + kDecodeTile) * L <= n_sym) {
+            // every span of the tile is whole: both chains run L steps in lockstep
+            double ax = P0.x, ay = P0.y, bx = P1.x, by = P1.y;
+            for (int k = L - 1; k >= 0; --k) {
+                const int ca = sector_of<EXACT>(ax, ay, t, cd);
+                const int cb = sector_of<EXACT>(bx, by, t, cd);
+                my0[k] = (uint8_t)ca;
+                my1[k] = (uint8_t)cb;
+                decode_step(ax, ay, t.Wr[ca], cd.inv_r);
+                decode_step(bx, by, t.Wr[cb], cd.inv_r);
+            }
+            f0 = !decode_finish<EXACT, VERIFY>(ax, ay, P0, my0, L, t, cd);
+            f1 = !decode_finish<EXACT, VERIFY>(bx, by, P1, my1, L, t, cd);
+            if (span_ok) {
+                span_ok[s * n_spans + j0 + lane] = f0 ? 0 : 1;
+                span_ok[s * n_spans + j0 + 64 + lane] = f1 ? 0 : 1;
+            }
+        } else {
+            // the stream's last tile: spans may be missing or short
+            for (int h = 0; h < kDecodeSpl; ++h) {
+                const int64_t jj = j0 + h * 64 + lane;
+                if (jj >= j0 + nsp) continue;
+                const int len = (int)min((int64_t)L, n_sym - jj * L);
+                uint8_t* my = h ? my1 : my0;
+                const double2 P = h ? P1 : P0;
+                double qx = P.x, qy = P.y;
+                for (int k = len - 1; k >= 0; --k) {
+                    const int c = sector_of<EXACT>(qx, qy, t, cd);
+                    my[k] = (uint8_t)c;
+                    decode_step(qx, qy, t.Wr[c], cd.inv_r);
+                }
+                const bool bad = !decode_finish<EXACT, VERIFY>(qx, qy, P, my, len, t, cd);
+                if (h) f1 = bad; else f0 = bad;
+                if (span_ok) span_ok[s * n_spans + jj] = bad ? 0 : 1;
+            }
+        }
+        count_flags(f0, n_failed);
+        count_flags(f1, n_failed);
         // the wave's LDS writes above precede its reads below (a wave's LDS
         // operations are performed in order)
         __builtin_amdgcn_wave_barrier();
         lds_to_bytes_wave(stage, g0, g1, sym, lane);
-        Pcur = Pnext;
+        P0 = N0;
+        P1 = N1;
     }
 }
 
@@ -274,11 +321,11 @@ extern "C" int fkv_cgr_decode_spans(const fkv_codec* c, const void* dev_table, c
         return FKV_ERR_INVALID_ARG;
     if (n_failed && !aligned(n_failed, 4)) return FKV_ERR_INVALID_ARG;
     const int64_t n_spans = (n_sym + c->L - 1) / c->L;
-    const int64_t wtps = (n_spans + 63) / 64;
+    const int64_t wtps = (n_spans + kDecodeTile - 1) / kDecodeTile;
     const int64_t n_wtiles = wtps * n_streams;
-    const int stage_bytes = (64 * c->L + 4 + 15) / 16 * 16;   // one wave tile's symbols, dword-shifted
-    const size_t shm = table_bytes(c->N) + (size_t)(kBlock / 64) * stage_bytes;
+    const int stage_bytes = (kDecodeTile * c->L + 4 + 15) / 16 * 16;   // one wave tile's symbols, dword-shifted
     const bool exact = needs_exact_sectors(c);
+    const size_t shm = staged_table_bytes(c->N, verify != 0, exact) + (size_t)(kBlock / 64) * stage_bytes;
     const dim3 grid((unsigned)min((int64_t)kMaxBlocks, (n_wtiles + kBlock / 64 - 1) / (kBlock / 64))), block(kBlock);
     const hipStream_t st = (hipStream_t)stream;
     const double2* P = (const double2*)points;
@@ -312,9 +359,9 @@ extern "C" int fkv_span_lookup(const fkv_codec* c, const void* dev_table, const 
     if (!aligned(q_stream, 4) || !aligned(q_token, 4)) return FKV_ERR_INVALID_ARG;
     if (n_failed && !aligned(n_failed, 4)) return FKV_ERR_INVALID_ARG;
     const int64_t n_spans = (n_sym + c->L - 1) / c->L;
-    const size_t shm = table_bytes(c->N);
-    const int64_t nb = blocks_for((n_q + kBlock - 1) / kBlock);
     const bool exact = needs_exact_sectors(c);
+    const size_t shm = staged_table_bytes(c->N, false, exact);
+    const int64_t nb = blocks_for((n_q + kBlock - 1) / kBlock);
     const hipStream_t st = (hipStream_t)stream;
     if (exact)
         hipLaunchKernelGGL((span_lookup_kernel<true>), dim3((unsigned)nb), dim3(kBlock), shm, st,

@@ -86,7 +86,7 @@ extern "C" int fkv_codec_fill_table(const fkv_codec* c, void* host_table)
     double* V = (double*)(base + fkv::table_off_V(N));
     double* W = (double*)(base + fkv::table_off_W(N));
     double* Wr = (double*)(base + fkv::table_off_Wr(N));
-    fkv::LutEntry* lut = (fkv::LutEntry*)(base + fkv::table_off_lut(N));
+    uint32_t* lut = (uint32_t*)(base + fkv::table_off_lut(N));
     for (int k = 0; k < N; ++k) {
         const double t = (2.0 * M_PI * (double)k) / (double)N;
         V[2 * k + 0] = cos(t);
@@ -96,38 +96,44 @@ extern "C" int fkv_codec_fill_table(const fkv_codec* c, void* host_table)
         Wr[2 * k + 0] = W[2 * k + 0] / r;
         Wr[2 * k + 1] = W[2 * k + 1] / r;
     }
-    // Sector boundaries (angle (k + 1/2) 2 pi / N) in pseudo-angle space,
-    // with the sector that starts at each of them.
+    // Sector boundaries (angle (k + 1/2) 2 pi / N) in bucket coordinates
+    // u = (P + 1) K + shift, with the sector that starts at each of them; the
+    // wrap boundary (sector 0 above it) sits exactly on a bucket edge.
+    const double K = (double)fkv::kLutPerUnit;
+    const double shift = fkv::lut_shift(N);
     std::vector<std::pair<double, int>> bnd;
     bnd.reserve(N);
     for (int k = 0; k < N; ++k) {
         const double a = ((double)k + 0.5) * 2.0 * M_PI / (double)N;
-        bnd.push_back({pseudo_angle(cos(a), sin(a)), (k + 1) % N});
+        const int above = (k + 1) % N;
+        double u = (pseudo_angle(cos(a), sin(a)) + 1.0) * K + shift;
+        if (above == 0) u = nearbyint(u);
+        bnd.push_back({u, above});
     }
     std::sort(bnd.begin(), bnd.end());
-    for (int i = 0; i < fkv::kLutBuckets; ++i) {
-        const double lo = -1.0 + (double)i / fkv::kLutPerUnit;
-        const double hi = -1.0 + (double)(i + 1) / fkv::kLutPerUnit;
-        // sector just above lo: the one started by the last boundary <= lo
-        // (before the first boundary: the sector that the first one ends)
+    for (int i = 0; i < fkv::kLutEntries; ++i) {
+        // sector just above the bucket's lower edge: the one started by the
+        // last boundary at or below it (before the first boundary: the
+        // sector that the first one ends)
         int c_lo = (bnd.front().second + N - 1) % N;
         for (const auto& b : bnd)
-            if (b.first <= lo) c_lo = b.second;
-        fkv::LutEntry e;
-        e.thr = INFINITY;
-        e.lo = (uint16_t)c_lo;
-        e.hi = (uint16_t)c_lo;
+            if (b.first <= (double)i) c_lo = b.second;
+        float thr = 2.0f;
         int found = 0;
         for (const auto& b : bnd) {
-            if (b.first > lo && b.first <= hi) {
+            if (b.first > (double)i && b.first < (double)(i + 1)) {
                 ++found;
-                e.thr = (float)b.first;
-                e.hi = (uint16_t)b.second;
+                if (b.second != c_lo + 1) return FKV_ERR_UNSUPPORTED;   // cannot happen: no wrap inside
+                thr = (float)(b.first - (double)i);
             }
         }
         if (found > 1) return FKV_ERR_UNSUPPORTED;  // cannot happen for N <= 256
-        lut[i] = e;
+        uint32_t w;
+        memcpy(&w, &thr, sizeof w);
+        lut[i] = (w & ~0xFFu) | (uint32_t)c_lo;
     }
+    memset(base + fkv::table_off_lut(N) + sizeof(uint32_t) * fkv::kLutEntries, 0,
+           fkv::kLutBytes - sizeof(uint32_t) * fkv::kLutEntries);
     return FKV_OK;
 }
 

@@ -1,6 +1,7 @@
 // fkv_internal.h -- private layout shared by libfkv's host code and kernels.
 #pragma once
 
+#include <math.h>
 #include <stddef.h>
 #include <stdint.h>
 
@@ -10,30 +11,48 @@ namespace fkv {
 // cell centres; decode finds a point's sector through a monotone
 // pseudo-angle  P = y/(|x|+|y|)  (x >= 0)  or  2 - y/(|x|+|y|)  (x < 0),
 // which runs from -1 (angle -pi/2) to 3 (angle 3pi/2).  P is cut into
-// kLutPerUnit buckets per unit; each bucket holds the sector at its lower
-// edge and, when one sector boundary falls inside it, that boundary and
-// the sector above it.  A sector is at least pi/N wide in P, wider than a
-// bucket for N <= 256, so a bucket never holds two boundaries.
+// kLutPerUnit buckets per unit; a sector is at least pi/N wide in P, wider
+// than a bucket for N <= 256, so a bucket holds at most one boundary.
+//
+// The bucket grid is shifted by lut_shift(N) buckets so that the boundary at
+// angle -pi/N, where the sector numbering wraps from N-1 to 0, falls on a
+// bucket edge: inside every bucket the sector above a boundary is then the
+// one below it plus one, and an entry is a single 32-bit word -- the
+// boundary's position within the bucket as an fp32 fraction (2 when the
+// bucket has none) whose low 8 mantissa bits are replaced by the sector at
+// the bucket's lower edge (the threshold moves by < 2^-15 of a bucket).
+//
+// The kernels evaluate the mirrored coordinate R = 1 - P, which is
+// copysign(1 - y/(|x|+|y|), x) (one fused multiply-add and a sign copy); the
+// bucket coordinate is u = (P + 1) kLutPerUnit + shift
+// = 2 kLutPerUnit + shift - R kLutPerUnit, in [0, 4 kLutPerUnit + 1).
 constexpr int kLutPerUnit = 128;
-constexpr int kLutBuckets = 4 * kLutPerUnit;
+constexpr int kLutEntries = 4 * kLutPerUnit + 1;
+constexpr size_t kLutBytes = (sizeof(uint32_t) * kLutEntries + 15) / 16 * 16;
 
-struct LutEntry {
-    float thr;      // P at the sector boundary inside this bucket, or +inf
-    uint16_t lo;    // sector for P < thr
-    uint16_t hi;    // sector for P >= thr
-};
-static_assert(sizeof(LutEntry) == 8, "LutEntry layout");
+// (P + 1) kLutPerUnit of the wrap boundary is c/(c+s) kLutPerUnit with
+// c = cos(pi/N), s = sin(pi/N); the shift lifts it to the next integer.
+inline double lut_shift(int N)
+{
+    const double s = sin(M_PI / (double)N), c = cos(M_PI / (double)N);
+    const double u = c / (c + s) * (double)kLutPerUnit;
+    return ceil(u) - u;
+}
 
-// Device table, one per alphabet, 16-byte aligned sections:
-//   [0,      16N)  V[c]   = (cos 2 pi c/N, sin 2 pi c/N)        double2
-//   [16N,    32N)  W[c]   = (1 - r) V[c]   (cell centres)        double2
-//   [32N,    48N)  Wr[c]  = W[c] / r                             double2
-//   [48N, 48N+4096) sector look-up table                         LutEntry[512]
-constexpr size_t table_off_V(int) { return 0; }
-constexpr size_t table_off_W(int N) { return (size_t)16 * N; }
-constexpr size_t table_off_Wr(int N) { return (size_t)32 * N; }
-constexpr size_t table_off_lut(int N) { return (size_t)48 * N; }
-constexpr size_t table_bytes(int N) { return (size_t)48 * N + sizeof(LutEntry) * kLutBuckets; }
+// Device table, one per alphabet, 16-byte aligned sections, ordered so that
+// the inverse map's fast path needs only the first two:
+//   [0,             16N)            Wr[c] = W[c] / r                double2
+//   [16N,           16N + B)        sector look-up table            uint32_t[513]
+//   [16N + B,       32N + B)        V[c]  = (cos 2 pi c/N, sin 2 pi c/N)
+//   [32N + B,       48N + B)        W[c]  = (1 - r) V[c]  (cell centres)
+// with B = kLutBytes.
+constexpr size_t table_off_Wr(int) { return 0; }
+constexpr size_t table_off_lut(int N) { return (size_t)16 * N; }
+constexpr size_t table_off_V(int N) { return (size_t)16 * N + kLutBytes; }
+constexpr size_t table_off_W(int N) { return (size_t)32 * N + kLutBytes; }
+constexpr size_t table_bytes(int N) { return (size_t)48 * N + kLutBytes; }
+// the prefix holding Wr and the look-up table
+constexpr size_t table_fast_bytes(int N) { return (size_t)16 * N + kLutBytes; }
 
 // Decode may take a sector straight from the look-up table only when every
 // valid point keeps a margin of at least this much (absolute, in the unit

@@ -11,6 +11,8 @@ import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "fkv.h")
+# bytes of the decode look-up table inside the codec's device table (513 words, 16-byte padded)
+LUT_BYTES = 2064
 
 
 @pytest.fixture(scope="module")
@@ -42,25 +44,38 @@ def test_codec_matches_oracle_bit_for_bit(F, orc):
             o = orc.Codec(N, scale)
             assert c.r_max == o.r_max and c.r == o.r and c.L == o.L, (N, scale)
             tab = c.host_table()
-            V = tab[:16 * N].view(np.float64).reshape(N, 2)
-            W = tab[16 * N:32 * N].view(np.float64).reshape(N, 2)
+            V = tab[16 * N + LUT_BYTES:32 * N + LUT_BYTES].view(np.float64).reshape(N, 2)
+            W = tab[32 * N + LUT_BYTES:48 * N + LUT_BYTES].view(np.float64).reshape(N, 2)
             assert np.array_equal(V, o.V) and np.array_equal(W, o.W), (N, scale)
     c = F.Codec(256, 0.98, 9)
     assert c.L == 9 and c.n_spans(100) == 12 and c.n_spans(0) == 0
 
 
+def _fma32(a, b, c):
+    """fp32 fused multiply-add: the exact product (two fp32 factors fit a double) plus c, rounded once."""
+    return (np.asarray(a, np.float64) * np.asarray(b, np.float64) + np.float64(c)).astype(np.float32)
+
+
 def _sector_fast_emulated(tab, N, q):
-    """NumPy emulation of the kernel's look-up-table sector search (fp32 pseudo-angle)."""
-    lut = tab[48 * N:].view(np.dtype([("thr", "<f4"), ("lo", "<u2"), ("hi", "<u2")]))
+    """NumPy emulation of the kernel's look-up-table sector search: the fp32 mirrored
+    pseudo-angle R = copysign(1 - y/(|x|+|y|), x), its bucket coordinate
+    u = 256 + shift - 128 R (shift puts the N-1 -> 0 boundary on a bucket edge), and the
+    bucket word (fp32 boundary fraction whose low byte holds the lower-edge sector)."""
+    lut = tab[16 * N:16 * N + 4 * 513].view("<u4")
     fx = q[:, 0].astype(np.float32)
     fy = q[:, 1].astype(np.float32)
-    s = np.abs(fx) + np.abs(fy)
-    d = fy / s
-    P = np.where(fx >= 0, d, np.float32(2) - d).astype(np.float32)
-    P = np.clip(P, -1, 2.99999).astype(np.float32)
-    idx = np.minimum(((P + 1) * 128).astype(np.int32), 511)
+    rs = (np.float32(1) / (np.abs(fx) + np.abs(fy))).astype(np.float32)
+    R = np.copysign(_fma32(-fy, rs, 1.0), fx)
+    R = np.clip(R, np.float32(-1.99999), np.float32(2)).astype(np.float32)
+    s, c = math.sin(math.pi / N), math.cos(math.pi / N)
+    u0 = c / (c + s) * 128
+    bias = np.float32(256 + (math.ceil(u0) - u0))
+    u = _fma32(R, -128.0, bias)
+    idx = u.astype(np.int32)
     e = lut[idx]
-    return np.where(P >= e["thr"], e["hi"], e["lo"]).astype(np.int64)
+    frac = (u - idx.astype(np.float32)).astype(np.float32)
+    thr = e.view(np.float32)
+    return ((e & 0xFF) + (frac >= thr)).astype(np.int64)
 
 
 @pytest.mark.parametrize("N", [3, 4, 5, 7, 16, 17, 64, 100, 256])
