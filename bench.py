@@ -46,9 +46,9 @@ def source_hash(*names):
 KERNEL_SOURCES = {
     "rvq_assign_encode": ("rvq_kernels.hip", "fkv_hip_common.h", "fkv_internal.h"),
     "rvq_assign": ("rvq_kernels.hip", "fkv_hip_common.h", "fkv_internal.h"),
-    "cgr_encode": ("cgr_kernels.hip", "fkv_hip_common.h", "fkv_internal.h"),
-    "cgr_decode": ("cgr_kernels.hip", "fkv_hip_common.h", "fkv_internal.h"),
-    "span_lookup": ("cgr_kernels.hip", "fkv_hip_common.h", "fkv_internal.h"),
+    "cgr_encode": ("cgr_kernels.hip", "cgr_device.h", "fkv_hip_common.h", "fkv_internal.h"),
+    "cgr_decode": ("cgr_kernels.hip", "cgr_device.h", "fkv_hip_common.h", "fkv_internal.h"),
+    "span_lookup": ("cgr_kernels.hip", "cgr_device.h", "fkv_hip_common.h", "fkv_internal.h"),
 }
 
 
