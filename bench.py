@@ -14,6 +14,9 @@ rates, the dominant kernel's roofline fraction and the CPU oracle's rate on the
 same workload are reported beside it.  The step is captured once as a HIP graph
 and replayed (no host launch overhead in the timed region); each kernel's
 average duration comes from a graph of back-to-back launches of that kernel.
+`reference_rates` gives what a library fp16 GEMM and a streaming elementwise
+kernel reach on the same device, and each roofline entry its achieved rate as
+a fraction of that (`frac_of_reference`) beside the datasheet fraction.
 """
 from __future__ import annotations
 
@@ -320,6 +323,42 @@ def cpu_baseline(cfg, groups, max_streams: int):
                       "time scaled to all streams" % (", ".join(frac), cfg.name)}
 
 
+def reference_rates(torch):
+    """What plain library kernels reach on this device, as context for the
+    roofline fractions: a dense fp16 GEMM (8192 x 8192 x 8192 through
+    torch.matmul) and a streaming elementwise kernel (torch.add over 1 GiB of
+    fp32: 1 GiB read, 1 GiB written).  Best of a few repetitions, events on the
+    current stream."""
+    def best_ms(f, reps=5):
+        f()
+        torch.cuda.synchronize()
+        best = float("inf")
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            f()
+            e1.record()
+            torch.cuda.synchronize()
+            best = min(best, e0.elapsed_time(e1))
+        return best
+
+    n = 8192
+    a = torch.randn((n, n), device="cuda", dtype=torch.float16)
+    b = torch.randn((n, n), device="cuda", dtype=torch.float16)
+    c = torch.empty((n, n), device="cuda", dtype=torch.float16)
+    gemm_ms = best_ms(lambda: torch.matmul(a, b, out=c))
+    del a, b, c
+    x = torch.ones(1 << 28, device="cuda", dtype=torch.float32)
+    y = torch.empty_like(x)
+    add_ms = best_ms(lambda: torch.add(x, 1.0, out=y))
+    del x, y
+    torch.cuda.empty_cache()
+    return {"fp16_gemm_tflops": round(2.0 * n ** 3 / (gemm_ms / 1e3) / 1e12, 1),
+            "fp16_gemm": "torch.matmul 8192^3, fp16 in and out",
+            "stream_gbs": round(2.0 * (1 << 30) / (add_ms / 1e3) / 1e9, 1),
+            "stream": "torch.add over 1 GiB fp32 (read + write)"}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -333,6 +372,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-read-stress", action="store_true",
                     help="skip the read-side measurements on the 144 x 131,072-token archive")
+    ap.add_argument("--no-reference-rates", action="store_true",
+                    help="skip the library GEMM and streaming-kernel reference rates")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="also run one streaming elementwise kernel (torch.neg) that reads and writes "
                          "this many MiB before the step: a kernel of known traffic for scaling HBM "
@@ -446,8 +487,18 @@ def main():
         "roofline": roof,
         "rooflines": rooflines,
         "next_rows": extra,
+        "reference_rates": None,
         "cpu_baseline": None,
     }
+    if not args.no_reference_rates:
+        ref = reference_rates(torch)
+        line["reference_rates"] = ref
+        # each kernel's achieved rate as a fraction of what the library kernel
+        # of the same kind reaches here
+        for n, r in rooflines.items():
+            r["frac_of_reference"] = round(r["achieved"] / (ref["fp16_gemm_tflops"] if r["bound"] == "mfma"
+                                                            else ref["stream_gbs"]), 4)
+        roof["frac_of_reference"] = rooflines[dominant]["frac_of_reference"]
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(cfg, groups, args.cpu_streams)
     print(json.dumps(line), flush=True)
