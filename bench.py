@@ -380,8 +380,8 @@ def main():
                          "byte counters")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py measures the path on one GPU; multi-GPU runs are not part of this build "
-              "(streams shard with no exchange, see DESIGN.md)", file=sys.stderr)
+        print("bench.py measures the path on one GPU; it has no multi-GPU mode (the streams are "
+              "independent and would shard across GPUs with no exchange)", file=sys.stderr)
         sys.exit(2)
 
     import torch

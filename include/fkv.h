@@ -41,7 +41,7 @@ extern "C" {
 typedef enum {
     FKV_OK = 0,
     FKV_ERR_INVALID_ARG = -1, /* a null pointer, a size or value out of range, a bad alignment */
-    FKV_ERR_UNSUPPORTED = -2, /* valid by the paper but outside what this build implements */
+    FKV_ERR_UNSUPPORTED = -2, /* valid by the paper but outside what this library implements */
     FKV_ERR_LAUNCH = -3,      /* the HIP runtime refused the launch (hipGetLastError) */
     FKV_ERR_NO_DEVICE = -4    /* no usable gfx950 device is current */
 } fkv_status;
