@@ -294,8 +294,10 @@ def read_stress(fkv, side, replays: int):
     }
 
 
-def cpu_baseline(cfg, groups, max_streams: int):
-    """The CPU oracle on (a sample of) the same step, all host cores, extrapolated per token."""
+def cpu_baseline(cfg, groups, max_streams: int, max_device_streams: int = 8):
+    """The CPU oracle on (a sample of) the same step, all host cores, extrapolated per token.
+    Inputs drawn on the device (the long-context workload) are sampled by copying the first
+    `max_device_streams` streams and all books to the host."""
     import oracle
 
     threads = oracle.default_threads()
@@ -303,9 +305,13 @@ def cpu_baseline(cfg, groups, max_streams: int):
     frac = []
     for gr in groups:
         if gr["host"] is None:
-            return None
-        xh, bh, sbh = gr["host"]
-        ns = min(gr["ns"], max_streams)
+            ns = min(gr["ns"], max_device_streams)
+            xh = gr["x"][:ns].cpu().numpy()
+            bh = gr["books"].cpu().numpy()
+            sbh = gr["sb"][:ns].cpu().numpy()
+        else:
+            xh, bh, sbh = gr["host"]
+            ns = min(gr["ns"], max_streams)
         t0 = time.perf_counter()
         o = oracle.rvq_assign(xh[:ns], bh, sbh[:ns], cfg.t_begin, cfg.t_end, want_residual=False,
                               want_gaps=False, threads=threads)
