@@ -25,14 +25,23 @@ namespace {
 
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 constexpr int kThreads = 256;
+// Accumulate: one 1024-thread block per (book, slice), so that enough member
+// tokens' loads are in flight to cover their latency (a block's tokens are
+// walked in 1024-task steps, each task waiting on its symbol, row and earlier
+// codewords).
+constexpr int kAccThreads = 1024;
 
 // One block per (book, 64-dimension slice): the block owns that slice of the
 // book's cluster sums, accumulates every member token of every stream of the
 // book into LDS (64-bit LDS atomics), then adds the slice to the global sums
 // with plain read-modify-writes (no other block touches it in this launch).
+// A cluster's row in LDS is dc + 1 words long: with an odd number of 8-byte
+// words per row, the same dimension of different clusters falls in different
+// banks (with dc words, every cluster's dimension e shared one bank, so the
+// atomics of a wave's tokens, which hit random clusters, serialised).
 constexpr int kSlice = 64;
 
-__global__ __launch_bounds__(kThreads) void kmeans_accumulate_kernel(
+__global__ __launch_bounds__(kAccThreads) void kmeans_accumulate_kernel(
     const _Float16* __restrict__ x, const _Float16* __restrict__ books, const int32_t* __restrict__ stream_book,
     const uint8_t* __restrict__ symbols, unsigned long long* __restrict__ sums, uint32_t* __restrict__ counts,
     int64_t n_streams, int64_t T, int64_t t_begin, int64_t Ta, int d, int S, int K, int stage)
@@ -42,42 +51,57 @@ __global__ __launch_bounds__(kThreads) void kmeans_accumulate_kernel(
     const int b = blockIdx.x / n_slices, slice = blockIdx.x - b * n_slices;
     const int e0 = slice * kSlice, dc = min(kSlice, d - e0);   // this block's dimensions [e0, e0 + dc)
     const int nch = dc / 8;
-    unsigned long long* ls = (unsigned long long*)lds;           // [K][dc]
-    uint32_t* lc = (uint32_t*)(ls + (size_t)K * dc);             // [K]
-    for (int i = threadIdx.x; i < K * dc; i += kThreads) ls[i] = 0;
-    for (int i = threadIdx.x; i < K; i += kThreads) lc[i] = 0;
-    __syncthreads();
-    for (int64_t s = 0; s < n_streams; ++s) {
-        if (stream_book[s] != b) continue;   // uniform across the block
-        for (int64_t task = threadIdx.x; task < Ta * nch; task += kThreads) {
-            const int64_t t = task / nch;
-            const int ch = (int)(task - t * nch);
-            const uint8_t* sym = symbols + (s * Ta + t) * S;
-            bool bad = false;
-            for (int st = 0; st <= stage; ++st) bad = bad || sym[st] >= K;
-            if (bad) continue;   // a symbol outside the book: the token is skipped
-            const half8 xv = *(const half8*)(x + (s * T + t_begin + t) * d + e0 + ch * 8);
-            double r[8];
+    const int pitch = dc + 1;                                    // words per cluster row
+    unsigned long long* ls = (unsigned long long*)lds;           // [K][pitch]
+    uint32_t* lc = (uint32_t*)(ls + (size_t)K * pitch);          // [K]
+    int* match = (int*)(lc + K);                                 // [kAccThreads]: streams of a chunk using book b
+    int* n_match = match + kAccThreads;
+    for (int i = threadIdx.x; i < K * pitch; i += kAccThreads) ls[i] = 0;
+    for (int i = threadIdx.x; i < K; i += kAccThreads) lc[i] = 0;
+    // The streams are scanned kAccThreads at a time, one per thread, and those
+    // of book b listed in LDS (their order does not matter: integer sums).
+    for (int64_t s0 = 0; s0 < n_streams; s0 += kAccThreads) {
+        if (threadIdx.x == 0) *n_match = 0;
+        __syncthreads();
+        if (s0 + threadIdx.x < n_streams && stream_book[s0 + threadIdx.x] == b)
+            match[atomicAdd(n_match, 1)] = (int)threadIdx.x;
+        __syncthreads();
+        const int nm = *n_match;
+        for (int m = 0; m < nm; ++m) {
+            const int64_t s = s0 + match[m];
+            // 32-bit task walk (the host checks that Ta * nch fits)
+            const int n_task = (int)(Ta * nch);
+            for (int task = threadIdx.x; task < n_task; task += kAccThreads) {
+                const int t = task / nch;
+                const int ch = task - t * nch;
+                const uint8_t* sym = symbols + (s * Ta + t) * S;
+                bool bad = false;
+                for (int st = 0; st <= stage; ++st) bad = bad || sym[st] >= K;
+                if (bad) continue;   // a symbol outside the book: the token is skipped
+                const half8 xv = *(const half8*)(x + (s * T + t_begin + t) * d + e0 + ch * 8);
+                double r[8];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) r[e] = (double)xv[e];
-            for (int st = 0; st < stage; ++st) {
-                const half8 c = *(const half8*)(books + (((int64_t)b * S + st) * K + sym[st]) * d + e0 + ch * 8);
+                for (int e = 0; e < 8; ++e) r[e] = (double)xv[e];
+                for (int st = 0; st < stage; ++st) {
+                    const half8 c = *(const half8*)(books + (((int64_t)b * S + st) * K + sym[st]) * d + e0 + ch * 8);
 #pragma unroll
-                for (int e = 0; e < 8; ++e) r[e] = r[e] - (double)c[e];
+                    for (int e = 0; e < 8; ++e) r[e] = r[e] - (double)c[e];
+                }
+                unsigned long long* dst = ls + (size_t)sym[stage] * pitch + ch * 8;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) atomicAdd(dst + e, (unsigned long long)(long long)ldexp(r[e], 24));
+                if (ch == 0 && slice == 0) atomicAdd(lc + sym[stage], 1u);
             }
-            unsigned long long* dst = ls + (size_t)sym[stage] * dc + ch * 8;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) atomicAdd(dst + e, (unsigned long long)(long long)ldexp(r[e], 24));
-            if (ch == 0 && slice == 0) atomicAdd(lc + sym[stage], 1u);
         }
+        __syncthreads();   // the list is rewritten for the next chunk
     }
-    __syncthreads();
-    for (int i = threadIdx.x; i < K * dc; i += kThreads) {
+    for (int i = threadIdx.x; i < K * dc; i += kAccThreads) {
         const int j = i / dc, e = i - j * dc;
-        if (ls[i]) sums[((int64_t)b * K + j) * d + e0 + e] += ls[i];
+        const unsigned long long v = ls[j * pitch + e];
+        if (v) sums[((int64_t)b * K + j) * d + e0 + e] += v;
     }
     if (slice == 0)
-        for (int j = threadIdx.x; j < K; j += kThreads)
+        for (int j = threadIdx.x; j < K; j += kAccThreads)
             if (lc[j]) counts[(int64_t)b * K + j] += lc[j];
 }
 
@@ -124,14 +148,15 @@ extern "C" int fkv_kmeans_accumulate(const fkv_rvq_desc* desc, const uint16_t* x
         !aligned(stream_book, 4))
         return FKV_ERR_INVALID_ARG;
     const int n_slices = (D.d + kSlice - 1) / kSlice;
-    const size_t shm = (size_t)D.K * std::min(kSlice, (int)D.d) * 8 + (size_t)D.K * 4;
+    if (Ta * (std::min(kSlice, (int)D.d) / 8) > 0x7fffffff) return FKV_ERR_UNSUPPORTED;
+    const size_t shm = (size_t)D.K * (std::min(kSlice, (int)D.d) + 1) * 8 + (size_t)D.K * 4 + (kAccThreads + 1) * 4;
     static std::once_flag once;
     std::call_once(once, [] {
         (void)hipFuncSetAttribute((const void*)kmeans_accumulate_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                  256 * kSlice * 8 + 256 * 4);
+                                  256 * (kSlice + 1) * 8 + 256 * 4 + (kAccThreads + 1) * 4);
     });
     (void)hipGetLastError();
-    hipLaunchKernelGGL(kmeans_accumulate_kernel, dim3((unsigned)(D.n_books * n_slices)), dim3(kThreads), shm,
+    hipLaunchKernelGGL(kmeans_accumulate_kernel, dim3((unsigned)(D.n_books * n_slices)), dim3(kAccThreads), shm,
                        (hipStream_t)stream, (const _Float16*)x_f16, (const _Float16*)books_f16, stream_book, symbols,
                        (unsigned long long*)sums, counts, D.n_streams, D.T, D.t_begin, Ta, D.d, D.S, D.K, stage);
     return launch_status();
