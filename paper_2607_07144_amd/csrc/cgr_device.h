@@ -101,11 +101,13 @@ __device__ inline int sector_fast(double qx, double qy, const uint32_t* __restri
     const float fx = (float)qx;
     const float fy = (float)qy;
     const float rs = __builtin_amdgcn_rcpf(fabsf(fx) + fabsf(fy));
-    // R = 1 - P = copysign(1 - y/(|x|+|y|), x), clamped into the table's
-    // range; zero or non-finite input gives NaN, which the clamp sends to -2
-    float R = __builtin_copysignf(__builtin_fmaf(-fy, rs, 1.0f), fx);
-    R = fminf(fmaxf(R, -1.99999f), 2.0f);
-    const float u = __builtin_fmaf(R, -(float)kLutPerUnit, lut_bias);   // in [0, 4 kLutPerUnit + 1)
+    // R = 1 - P = copysign(1 - y/(|x|+|y|), x).  |y| rs <= 1 up to rounding,
+    // so u stays within [-2^-14, 4 kLutPerUnit + 1 + 2^-14): truncation sends
+    // a slightly negative u to bucket 0, and the table repeats its last bucket
+    // in its padding; zero or non-finite input gives NaN, which converts to
+    // bucket 0.  No clamp is needed.
+    const float R = __builtin_copysignf(__builtin_fmaf(-fy, rs, 1.0f), fx);
+    const float u = __builtin_fmaf(R, -(float)kLutPerUnit, lut_bias);
     const uint32_t e = lut[(int)u];
     // lower-edge sector, plus one when the point lies past the bucket's boundary
     return (int)(e & 0xFFu) + (__builtin_amdgcn_fractf(u) >= __uint_as_float(e) ? 1 : 0);

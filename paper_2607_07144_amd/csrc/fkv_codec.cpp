@@ -132,8 +132,10 @@ extern "C" int fkv_codec_fill_table(const fkv_codec* c, void* host_table)
         memcpy(&w, &thr, sizeof w);
         lut[i] = (w & ~0xFFu) | (uint32_t)c_lo;
     }
-    memset(base + fkv::table_off_lut(N) + sizeof(uint32_t) * fkv::kLutEntries, 0,
-           fkv::kLutBytes - sizeof(uint32_t) * fkv::kLutEntries);
+    // the section's padding repeats the last bucket: a coordinate that rounds
+    // just past the range's upper end (the direction -pi/2 approached with
+    // x < 0) reads the bucket it belongs to, with no clamp in the kernels
+    for (size_t i = fkv::kLutEntries; i < fkv::kLutBytes / sizeof(uint32_t); ++i) lut[i] = lut[fkv::kLutEntries - 1];
     return FKV_OK;
 }
 

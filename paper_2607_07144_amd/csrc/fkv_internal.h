@@ -29,6 +29,7 @@ namespace fkv {
 constexpr int kLutPerUnit = 128;
 constexpr int kLutEntries = 4 * kLutPerUnit + 1;
 constexpr size_t kLutBytes = (sizeof(uint32_t) * kLutEntries + 15) / 16 * 16;
+static_assert(kLutBytes / sizeof(uint32_t) >= kLutEntries + 1, "the look-up table needs a padding entry");
 
 // (P + 1) kLutPerUnit of the wrap boundary is c/(c+s) kLutPerUnit with
 // c = cos(pi/N), s = sin(pi/N); the shift lifts it to the next integer.
