@@ -243,8 +243,9 @@ def next_rows(fkv, cfg, groups, side, replays: int):
 def read_stress(fkv, side, replays: int):
     """Read side at HBM scale: the 144-stream x 131,072-token archive (2 symbols per token, N = 256).
     Bulk decode rotates over 4 copies of the points so that consecutive launches do not hit the
-    memory-side cache; 2^20 random lookups; the per-position retrieval index (build and one suffix
-    scan of 16 bytes per position)."""
+    memory-side cache; 2^20 random lookups, beside a library gather of the same queries' points (the
+    random-transaction bound); the per-position retrieval index (build and one suffix scan of 16
+    bytes per position)."""
     import torch
     from paper_2607_07144_amd import workloads
 
@@ -274,6 +275,7 @@ def read_stress(fkv, side, replays: int):
         t_tr = time_graph(lambda: fkv.fkv_trajectory(codec, sym, traj=traj), 2, replays, side)
         t_sc = time_graph(lambda: fkv.fkv_suffix_search(codec, traj, query, max_hits=1 << 16, hits=hits,
                                                         n_hits=nh), 4, replays, side)
+        t_ga = gather_reference(pts, qs_h, qt_h, c["S"], L=codec.L, stream=side)
     n_pos = ns * n_sym
     dec_bytes = n_pos + pts.numel() * 8
     L = codec.L
@@ -286,12 +288,43 @@ def read_stress(fkv, side, replays: int):
         "bulk_decode": {"avg_launch_us": round(t_dec * 1e6, 2), "symbols_per_s": round(n_pos / t_dec, 1),
                         "roofline": hbm(dec_bytes, t_dec), "rotation": 4},
         "lookup": {"queries": int(qs_h.size), "avg_launch_us": round(t_lk * 1e6, 2),
-                   "lookups_per_s": round(qs_h.size / t_lk, 1), "roofline": hbm(lk_bytes, t_lk)},
+                   "lookups_per_s": round(qs_h.size / t_lk, 1), "roofline": hbm(lk_bytes, t_lk),
+                   "gather_reference": {"op": "torch.index_select of the queries' 16-byte points as complex128 (same archive)",
+                                        "avg_launch_us": round(t_ga * 1e6, 2),
+                                        "gathers_per_s": round(qs_h.size / t_ga, 1)},
+                   "frac_of_reference": round(t_ga / t_lk, 4)},
         "index_build": {"avg_launch_us": round(t_tr * 1e6, 2), "positions_per_s": round(n_pos / t_tr, 1),
                         "roofline": hbm(n_pos * 17, t_tr)},
         "suffix_scan": {"avg_launch_us": round(t_sc * 1e6, 2), "positions_per_s": round(n_pos / t_sc, 1),
                         "query_len": 3, "roofline": hbm(n_pos * 16, t_sc)},
     }
+
+
+def gather_reference(pts, qs_h, qt_h, S: int, L: int, stream, reps: int = 8, replays: int = 5):
+    """The random-transaction bound of the lookups: a library gather (torch.index_select) of the
+    same queries' 16-byte points from the same archive, with no decoding.  Each query of this
+    archive touches one span, so lookups/s and gathers/s compare one to one.  Timed eagerly:
+    `reps` back-to-back gathers between events on `stream`, best of `replays`."""
+    import torch
+
+    n_spans = pts.shape[1]
+    rows = qs_h.astype(np.int64) * n_spans + (qt_h.astype(np.int64) * S) // L
+    # one complex128 element per point, so that each gathered element is one 16-byte load
+    flat = pts.reshape(-1, 2).view(torch.complex128).reshape(-1)
+    idx = torch.from_numpy(rows).to(flat.device)
+    dst = torch.empty(idx.numel(), dtype=flat.dtype, device=flat.device)
+    best = float("inf")
+    with torch.cuda.stream(stream):
+        torch.index_select(flat, 0, idx, out=dst)
+        for _ in range(replays):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(reps):
+                torch.index_select(flat, 0, idx, out=dst)
+            e1.record(stream)
+            e1.synchronize()
+            best = min(best, e0.elapsed_time(e1) / 1e3 / reps)
+    return best
 
 
 def cpu_baseline(cfg, groups, max_streams: int, max_device_streams: int = 8):
