@@ -56,17 +56,21 @@ def _fma32(a, b, c):
     return (np.asarray(a, np.float64) * np.asarray(b, np.float64) + np.float64(c)).astype(np.float32)
 
 
+LUT_BYTES = (4 * 513 + 15) // 16 * 16   # 513 bucket words, padded to 16 bytes
+
+
 def _sector_fast_emulated(tab, N, q):
     """NumPy emulation of the kernel's look-up-table sector search: the fp32 mirrored
     pseudo-angle R = copysign(1 - y/(|x|+|y|), x), its bucket coordinate
     u = 256 + shift - 128 R (shift puts the N-1 -> 0 boundary on a bucket edge), and the
-    bucket word (fp32 boundary fraction whose low byte holds the lower-edge sector)."""
-    lut = tab[16 * N:16 * N + 4 * 513].view("<u4")
+    bucket word (fp32 boundary fraction whose low byte holds the lower-edge sector).  u is not
+    clamped: it lies in [-2^-14, 513 + 2^-14), truncation sends a slightly negative u to
+    bucket 0, and the entries past the last bucket repeat it."""
+    lut = tab[16 * N:16 * N + LUT_BYTES].view("<u4")
     fx = q[:, 0].astype(np.float32)
     fy = q[:, 1].astype(np.float32)
     rs = (np.float32(1) / (np.abs(fx) + np.abs(fy))).astype(np.float32)
     R = np.copysign(_fma32(-fy, rs, 1.0), fx)
-    R = np.clip(R, np.float32(-1.99999), np.float32(2)).astype(np.float32)
     s, c = math.sin(math.pi / N), math.cos(math.pi / N)
     u0 = c / (c + s) * 128
     bias = np.float32(256 + (math.ceil(u0) - u0))
@@ -106,6 +110,25 @@ def test_sector_table_agrees_with_oracle_cells(F, orc, N):
     got = _sector_fast_emulated(tab, N, q)
     want = np.array([orc.cell(o, a, b) for a, b in q])
     assert np.array_equal(got, want)
+
+
+@pytest.mark.parametrize("N", [4, 8, 16, 64, 256])
+def test_sector_table_edges(F, orc, N):
+    """The ends of the bucket range: points on the axes (R = +-1, 0 and +-2, including a signed
+    zero x, which selects the first or the last bucket) give the oracle's cell, and the table's
+    padding words repeat its last bucket, so the unclamped bucket index stays inside the table."""
+    c = F.Codec(N, 0.98)
+    o = orc.Codec(N, 0.98)
+    tab = c.host_table()
+    lut = tab[16 * N:16 * N + LUT_BYTES].view("<u4")
+    assert np.all(lut[513:] == lut[512])
+    pts = []
+    for a in (1e-3, 0.25, 0.5, 1.0):
+        pts += [(a, 0.0), (-a, 0.0), (0.0, a), (0.0, -a), (-0.0, -a), (-0.0, a)]
+    q = np.array(pts, dtype=np.float64)
+    got = _sector_fast_emulated(tab, N, q)
+    want = np.array([orc.cell(o, a, b) for a, b in q])
+    assert np.array_equal(got, want), (got, want)
 
 
 def test_invalid_arguments_are_rejected_on_the_host(F):

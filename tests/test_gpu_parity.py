@@ -56,6 +56,28 @@ def test_encode_decode_parity(fkv, orc, N, scale, Lo):
             assert host(ok).all() and int(host(nf)[0]) == 0
 
 
+@pytest.mark.parametrize("N", [3, 4, 8, 16, 64, 256])
+def test_constant_spans_every_vertex_direction(fkv, orc, N):
+    """Spans of one repeated symbol put the stored point, and every point of its backward walk,
+    on the ray of that symbol's vertex: for N divisible by 4 some of these lie on the axes, where
+    the pseudo-angle reaches the ends of the sector table's bucket range.  Every symbol, and
+    every symbol followed by its neighbours, decodes back exactly."""
+    c = fkv.Codec(N, 0.98)
+    o = orc.Codec(N, 0.98)
+    L = c.L
+    rows = [np.full(L, v, dtype=np.uint8) for v in range(N)]
+    rows += [np.array([(v + k) % N for k in range(L)], dtype=np.uint8) for v in range(N)]
+    rows += [np.array([(v - k) % N for k in range(L)], dtype=np.uint8) for v in range(N)]
+    sym = np.concatenate(rows)[None, :]
+    pts = fkv.fkv_cgr_encode_spans(c, dev(sym))
+    want = orc.encode(o, sym)
+    assert host(pts).view(np.uint64).tobytes() == want.view(np.uint64).tobytes()
+    nf = torch.zeros(1, dtype=torch.int32, device="cuda")
+    dec = fkv.fkv_cgr_decode_spans(c, pts, sym.shape[1], n_failed=nf)
+    assert np.array_equal(host(dec), sym)
+    assert int(host(nf)[0]) == 0
+
+
 def test_decode_failure_flags_match_oracle(fkv, orc):
     for N in (16, 64, 256):
         c = fkv.Codec(N)
