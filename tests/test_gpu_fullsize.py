@@ -105,3 +105,31 @@ def test_read_stress_archive(fkv, orc):
     # the first 4096 lookups also through the oracle
     oout, ost, _ = orc.lookup(oc, host(pts), n_sym, c["S"], qs_h[:4096], qt_h[:4096])
     assert np.array_equal(host(out[:4096]), oout) and not ost.any()
+
+
+@pytest.mark.parametrize("N,half", [(3, True), (16, False), (64, False), (256, False)])
+def test_capacity_at_scale(fkv, orc, N, half):
+    """Sec. 1 capacity claim at scale: about 44/log2(1/r) symbols per double.  At
+    L = floor(44/log2(1/r)) over 2^22 random spans (r = 1/2 for the triangle, 0.98 r_N
+    otherwise) every span decodes back and passes its anchor check; a sample of the points is
+    bit-identical to the oracle's."""
+    r_scale = 0.5 / orc.r_max(N) if half else 0.98
+    c = fkv.Codec(N, r_scale)
+    oc = orc.Codec(N, r_scale)
+    assert (c.r, c.L) == (oc.r, oc.L)
+    n_spans = 1 << 22
+    ns = 4
+    n_sym = n_spans // ns * c.L
+    g = torch.Generator(device="cuda")
+    g.manual_seed(4242 + N)
+    sym = torch.randint(0, N, (ns, n_sym), dtype=torch.uint8, device="cuda", generator=g)
+    pts = fkv.fkv_cgr_encode_spans(c, sym)
+    nf = torch.zeros(1, dtype=torch.int32, device="cuda")
+    dec = fkv.fkv_cgr_decode_spans(c, pts, n_sym, n_failed=nf)
+    assert int(nf.item()) == 0
+    assert torch.equal(dec, sym)
+    del dec
+    # oracle on 2048 spans of the last stream, whole spans from its end
+    k = 2048
+    tail = host(sym[ns - 1, n_sym - k * c.L:]).reshape(1, -1)
+    assert np.array_equal(host(pts[ns - 1, -k:]), orc.encode(oc, tail)[0])
