@@ -23,7 +23,7 @@ def _search(fkv, codec, traj, q, verify, max_hits=1 << 16):
     return sorted(map(tuple, got.tolist())), n, int(nc.item())
 
 
-@pytest.mark.parametrize("N,W", [(16, 0), (64, 0), (256, 0), (3, 64), (256, 11)])
+@pytest.mark.parametrize("N,W", [(16, 0), (64, 0), (256, 0), (3, 64), (256, 11), (256, 1), (64, 16), (64, 17)])
 def test_trajectory_matches_oracle(fkv, orc, N, W):
     rng = np.random.default_rng(N + W)
     sym = rng.integers(0, N, (5, 1000 + 37), dtype=np.uint8)     # a ragged last tile
