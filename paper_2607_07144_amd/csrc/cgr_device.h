@@ -109,8 +109,17 @@ __device__ inline int sector_fast(double qx, double qy, const uint32_t* __restri
     const float R = __builtin_copysignf(__builtin_fmaf(-fy, rs, 1.0f), fx);
     const float u = __builtin_fmaf(R, -(float)kLutPerUnit, lut_bias);
     const uint32_t e = lut[(int)u];
-    // lower-edge sector, plus one when the point lies past the bucket's boundary
-    return (int)(e & 0xFFu) + (__builtin_amdgcn_fractf(u) >= __uint_as_float(e) ? 1 : 0);
+    // lower-edge sector (the word's low byte), plus one when the point lies
+    // past the bucket's boundary: the compare sets the carry that an add with
+    // byte-0 operand select consumes, so no separate mask of the low byte
+    const float f = __builtin_amdgcn_fractf(u);
+    uint32_t c;
+    asm("v_cmp_ge_f32 vcc, %1, %2\n\t"
+        "v_addc_co_u32_sdwa %0, vcc, %3, %2, vcc dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_0"
+        : "=v"(c)
+        : "v"(f), "v"(e), "v"(0u)
+        : "vcc");
+    return (int)c;
 }
 
 // Exact nearest cell centre, lowest index on exact ties (used when the margin
