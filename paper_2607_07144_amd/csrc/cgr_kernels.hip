@@ -145,6 +145,24 @@ __device__ inline bool decode_finish(double qx, double qy, const double2 P, cons
     return ok;
 }
 
+// Two independent backward walks of `len` steps (LC > 0: the length fixed at
+// compile time, so the loop unrolls fully), symbols into my0 / my1.
+template <int LC, bool EXACT>
+__device__ __forceinline__ void walk_two(double& ax, double& ay, double& bx, double& by, uint8_t* my0, uint8_t* my1,
+                                         int len, const Tables& t, const CodecArgs& cd)
+{
+    const int n = LC > 0 ? LC : len;
+#pragma unroll
+    for (int k = n - 1; k >= 0; --k) {
+        const int ca = sector_of<EXACT>(ax, ay, t, cd);
+        const int cb = sector_of<EXACT>(bx, by, t, cd);
+        my0[k] = (uint8_t)ca;
+        my1[k] = (uint8_t)cb;
+        decode_step(ax, ay, t.Wr[ca], cd.inv_r);
+        decode_step(bx, by, t.Wr[cb], cd.inv_r);
+    }
+}
+
 template <bool EXACT, bool VERIFY>
 __global__ __launch_bounds__(kBlock, 8) void cgr_decode_kernel(
     const double2* __restrict__ pts, uint8_t* __restrict__ sym, uint8_t* __restrict__ span_ok,
@@ -191,14 +209,10 @@ __global__ __launch_bounds__(kBlock, 8) void cgr_decode_kernel(
         if (nsp == kDecodeTile && (j0 + kDecodeTile) * L <= n_sym) {
             // every span of the tile is whole: both chains run L steps in lockstep
             double ax = P0.x, ay = P0.y, bx = P1.x, by = P1.y;
-            for (int k = L - 1; k >= 0; --k) {
-                const int ca = sector_of<EXACT>(ax, ay, t, cd);
-                const int cb = sector_of<EXACT>(bx, by, t, cd);
-                my0[k] = (uint8_t)ca;
-                my1[k] = (uint8_t)cb;
-                decode_step(ax, ay, t.Wr[ca], cd.inv_r);
-                decode_step(bx, by, t.Wr[cb], cd.inv_r);
-            }
+            if (L == 6)   // N = 256 at 0.98 r_N: a fixed length, fully unrolled
+                walk_two<6, EXACT>(ax, ay, bx, by, my0, my1, L, t, cd);
+            else
+                walk_two<0, EXACT>(ax, ay, bx, by, my0, my1, L, t, cd);
             f0 = !decode_finish<EXACT, VERIFY>(ax, ay, P0, my0, L, t, cd);
             f1 = !decode_finish<EXACT, VERIFY>(bx, by, P1, my1, L, t, cd);
             if (span_ok) {
