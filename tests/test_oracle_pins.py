@@ -499,3 +499,27 @@ def test_window_and_sizes(facts):
     assert round(100 * (w.SINKS + w.RECENT) / g.T, 1) == win["exact_percent"]
     assert g.scalars_per_token() == facts["gpt2_kv_scalars_per_token"]["value"]
     assert 2 * g.scalars_per_token() == facts["fp16_bytes_per_token"]["value"]
+
+
+@pytest.mark.parametrize("delta,accepted", [(0.0, True), (0.01, True), (2.0 ** -6, True),
+                                            (2.0 ** -6 * (1 + 2.0 ** -20), False), (0.05, False),
+                                            (0.5, False)])
+def test_anchor_band_closed_form(orc, delta, accepted):
+    """Anchored backward reconstruction (Sec. 1): a span is accepted iff its backward walk ends
+    within 2^-6 of the anchor (the band is this build's reading; the paper names the anchor
+    check without a tolerance).  N = 3, r = 1/2, L = 44: the span 0^L encodes to (1 - 2^-L, 0)
+    exactly.  Displacing the stored y by delta 2^-L keeps every backward step in cell 0
+    (q <- 2q - (1, 0): x walks 1 - 2^-k exactly, y doubles), so the walk ends at exactly
+    (0, delta): the anchor residual is delta and the decision is delta <= 2^-6."""
+    c = orc.Codec(3, r_scale=1.0)
+    L = c.L
+    assert (c.r, L) == (0.5, 44)
+    sym = np.zeros((1, L), np.uint8)
+    pts = orc.encode(c, sym)
+    assert pts[0, 0].tolist() == [1.0 - 2.0 ** -L, 0.0]
+    bad = pts.copy()
+    bad[0, 0, 1] = math.ldexp(delta, -L)
+    dec, ok, nf, res = orc.decode(c, bad, L)
+    assert np.array_equal(dec, sym)
+    assert res[0, 0] == delta
+    assert bool(ok[0, 0]) == accepted and nf == (0 if accepted else 1)
