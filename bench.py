@@ -271,11 +271,21 @@ def read_stress(fkv, side, replays: int):
 
     with torch.cuda.stream(side):
         t_dec = time_graph(decode, 8, replays, side)
-        t_lk = time_graph(lambda: fkv.fkv_span_lookup(codec, pts, n_sym, c["S"], qs, qt, out=out), 4, replays, side)
+        rot[0] = 0
+
+        def lookup():
+            fkv.fkv_span_lookup(codec, copies[rot[0] % 4], n_sym, c["S"], qs, qt, out=out)
+            rot[0] += 1
+
+        t_lk = time_graph(lookup, 8, replays, side)
         t_tr = time_graph(lambda: fkv.fkv_trajectory(codec, sym, traj=traj), 2, replays, side)
         t_sc = time_graph(lambda: fkv.fkv_suffix_search(codec, traj, query, max_hits=1 << 16, hits=hits,
                                                         n_hits=nh), 4, replays, side)
-        t_ga = gather_reference(pts, qs_h, qt_h, c["S"], L=codec.L, stream=side)
+        t_ga = gather_reference(copies, qs_h, qt_h, c["S"], L=codec.L, stream=side)
+    lk_err = int((out != sym.view(ns, -1, c["S"])[qs.long(), qt.long()]).any(dim=1).sum().item())
+    nf = torch.zeros(1, dtype=torch.int32, device="cuda")
+    fkv.fkv_cgr_decode_spans(codec, pts, n_sym, symbols=dec, n_failed=nf)
+    dec_err = int((dec != sym).sum().item())
     n_pos = ns * n_sym
     dec_bytes = n_pos + pts.numel() * 8
     L = codec.L
@@ -286,10 +296,13 @@ def read_stress(fkv, side, replays: int):
     return {
         "archive": "%d streams x %d symbols, N=%d, L=%d" % (ns, n_sym, c["N"], L),
         "bulk_decode": {"avg_launch_us": round(t_dec * 1e6, 2), "symbols_per_s": round(n_pos / t_dec, 1),
-                        "roofline": hbm(dec_bytes, t_dec), "rotation": 4},
+                        "roofline": hbm(dec_bytes, t_dec), "rotation": 4, "decode_failed_spans": int(nf.item()),
+                        "roundtrip_symbol_errors": dec_err},
         "lookup": {"queries": int(qs_h.size), "avg_launch_us": round(t_lk * 1e6, 2),
                    "lookups_per_s": round(qs_h.size / t_lk, 1), "roofline": hbm(lk_bytes, t_lk),
-                   "gather_reference": {"op": "torch.index_select of the queries' 16-byte points as complex128 (same archive)",
+                   "rotation": 4, "lookup_errors": lk_err,
+                   "gather_reference": {"op": "torch.index_select of the queries' 16-byte points as complex128 "
+                                              "(same archive, same 4-copy rotation)",
                                         "avg_launch_us": round(t_ga * 1e6, 2),
                                         "gathers_per_s": round(qs_h.size / t_ga, 1)},
                    "frac_of_reference": round(t_ga / t_lk, 4)},
@@ -300,66 +313,153 @@ def read_stress(fkv, side, replays: int):
     }
 
 
-def gather_reference(pts, qs_h, qt_h, S: int, L: int, stream, reps: int = 8, replays: int = 5):
+def gather_reference(copies, qs_h, qt_h, S: int, L: int, stream, reps: int = 8, replays: int = 5):
     """The random-transaction bound of the lookups: a library gather (torch.index_select) of the
-    same queries' 16-byte points from the same archive, with no decoding.  Each query of this
-    archive touches one span, so lookups/s and gathers/s compare one to one.  Timed eagerly:
+    same queries' 16-byte points from the same archive, with no decoding, rotating over the same
+    copies as the lookups (so that neither is served from the memory-side cache).  Each query of
+    this archive touches one span, so lookups/s and gathers/s compare one to one.  Timed eagerly:
     `reps` back-to-back gathers between events on `stream`, best of `replays`."""
     import torch
 
-    n_spans = pts.shape[1]
+    n_spans = copies[0].shape[1]
     rows = qs_h.astype(np.int64) * n_spans + (qt_h.astype(np.int64) * S) // L
     # one complex128 element per point, so that each gathered element is one 16-byte load
-    flat = pts.reshape(-1, 2).view(torch.complex128).reshape(-1)
-    idx = torch.from_numpy(rows).to(flat.device)
-    dst = torch.empty(idx.numel(), dtype=flat.dtype, device=flat.device)
+    flats = [p.reshape(-1, 2).view(torch.complex128).reshape(-1) for p in copies]
+    idx = torch.from_numpy(rows).to(flats[0].device)
+    dst = torch.empty(idx.numel(), dtype=flats[0].dtype, device=flats[0].device)
     best = float("inf")
     with torch.cuda.stream(stream):
-        torch.index_select(flat, 0, idx, out=dst)
+        torch.index_select(flats[0], 0, idx, out=dst)
         for _ in range(replays):
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record(stream)
-            for _ in range(reps):
-                torch.index_select(flat, 0, idx, out=dst)
+            for k in range(reps):
+                torch.index_select(flats[k % len(flats)], 0, idx, out=dst)
             e1.record(stream)
             e1.synchronize()
             best = min(best, e0.elapsed_time(e1) / 1e3 / reps)
     return best
 
 
-def cpu_baseline(cfg, groups, max_streams: int, max_device_streams: int = 8):
-    """The CPU oracle on (a sample of) the same step, all host cores, extrapolated per token.
-    Inputs drawn on the device (the long-context workload) are sampled by copying the first
-    `max_device_streams` streams and all books to the host."""
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _span_prefix(T_arch: int, S: int, L: int, want: int) -> int:
+    """The largest token count <= want whose symbols fill whole spans (all tokens if want >= T_arch)."""
+    if want >= T_arch:
+        return T_arch
+    n = want
+    while n > 0 and (n * S) % L:
+        n -= 1
+    return max(n, 1)
+
+
+def cpu_baseline(cfg, groups, max_streams: int, max_tokens: int, st_streams: int, st_tokens: int):
+    """The CPU oracle on a bounded sample of the same step, timed on this host, and the oracle as
+    checker of the GPU's outputs on that sample.
+
+    Sample: the first `max_streams` streams of each group (the first layer's streams: streams are
+    ordered layer-major) on their first `max_tokens` archived tokens (a whole number of spans).
+    The all-cores leg runs the full step there (RVQ, encode, decode, and the step's lookups that
+    fall in the sample) with OpenMP over streams; the single-thread leg runs RVQ, encode and decode
+    on `st_streams` x `st_tokens` of the same sample.  Both are scaled per stream-token (lookups
+    per query) to the whole workload.  As checker, the all-cores leg takes the GPU's symbols as
+    teacher (near-ties within 1e-5 relative are accepted and counted per stage; any other
+    difference is a hard mismatch) and compares the GPU's points, decoded symbols and lookups bit
+    for bit."""
+    import torch
     import oracle
 
     threads = oracle.default_threads()
-    t_total = 0.0
-    frac = []
-    for gr in groups:
-        if gr["host"] is None:
-            ns = min(gr["ns"], max_device_streams)
-            xh = gr["x"][:ns].cpu().numpy()
-            bh = gr["books"].cpu().numpy()
-            sbh = gr["sb"][:ns].cpu().numpy()
-        else:
-            xh, bh, sbh = gr["host"]
-            ns = min(gr["ns"], max_streams)
+    t_all = t_one = 0.0
+    sample, check = [], []
+    for gi, gr in enumerate(groups):
+        g, L = gr["g"], gr["codec"].L
+        ns = min(gr["ns"], max_streams)
+        nt = _span_prefix(cfg.T_arch, g.S, L, max_tokens)
+        n_sym = nt * g.S
+        xh = gr["x"][:ns, :cfg.t_begin + nt].cpu().numpy() if gr["host"] is None else gr["host"][0][:ns, :cfg.t_begin + nt]
+        bh = gr["books"].cpu().numpy()
+        sbh = gr["sb"][:ns].cpu().numpy()
+        gsym = gr["sym"][:ns, :n_sym].cpu().numpy()
+        gpts = gr["pts"][:ns, :(n_sym + L - 1) // L].cpu().numpy()
+        gdec = gr["dec"][:ns, :n_sym].cpu().numpy()
+        keep = (gr["qs_h"] < ns) & (gr["qt_h"] < nt)
+        qs, qt = gr["qs_h"][keep].astype(np.uint32), gr["qt_h"][keep].astype(np.uint32)
+        gout = gr["out"].cpu().numpy()[keep]
+        oc = oracle.Codec(g.N, g.r_scale)
+
         t0 = time.perf_counter()
-        o = oracle.rvq_assign(xh[:ns], bh, sbh[:ns], cfg.t_begin, cfg.t_end, want_residual=False,
-                              want_gaps=False, threads=threads)
-        oc = oracle.Codec(gr["g"].N, gr["g"].r_scale)
+        o = oracle.rvq_assign(xh, bh, sbh, cfg.t_begin, cfg.t_begin + nt, force=gsym, force_tol=1e-5,
+                              want_residual=False, want_gaps=True, threads=threads)
         pts = oracle.encode(oc, o["symbols"], threads=threads)
-        oracle.decode(oc, pts, gr["n_sym"], threads=threads)
-        keep = gr["qs_h"] < ns
-        oracle.lookup(oc, pts, gr["n_sym"], gr["g"].S, gr["qs_h"][keep].astype(np.uint32),
-                      gr["qt_h"][keep].astype(np.uint32), threads=threads)
-        t_total += (time.perf_counter() - t0) * gr["ns"] / ns
-        frac.append("%d/%d streams" % (ns, gr["ns"]))
-    return {"value": cfg.batch * cfg.T_arch / t_total, "unit": "archived tokens/s", "cores": threads,
-            "kind": "oracle",
-            "sample": "%s of %s (full step: RVQ, encode, decode, lookups on the sampled streams), "
-                      "time scaled to all streams" % (", ".join(frac), cfg.name)}
+        dsym, _, nfail, _ = oracle.decode(oc, pts, n_sym, threads=threads)
+        t1 = time.perf_counter()
+        lout, _, _ = oracle.lookup(oc, pts, n_sym, g.S, qs, qt, threads=threads)
+        t2 = time.perf_counter()
+        scale_tok = gr["ns"] * cfg.T_arch / (ns * nt)
+        t_all += (t1 - t0) * scale_tok + (t2 - t1) * gr["qs_h"].size / max(1, int(keep.sum()))
+
+        sn, stt = min(ns, st_streams), _span_prefix(cfg.T_arch, g.S, L, st_tokens)
+        t0 = time.perf_counter()
+        o1 = oracle.rvq_assign(xh[:sn, :cfg.t_begin + stt], bh, sbh[:sn], cfg.t_begin, cfg.t_begin + stt,
+                               want_residual=False, want_gaps=False, threads=1)
+        p1 = oracle.encode(oc, o1["symbols"], threads=1)
+        oracle.decode(oc, p1, stt * g.S, threads=1)
+        t_one += (time.perf_counter() - t0) * gr["ns"] * cfg.T_arch / (sn * stt)
+
+        gaps = o["gaps"].reshape(ns, nt, g.S)
+        check.append({
+            "group": gi, "streams": ns, "tokens_per_stream": nt,
+            "assignments_per_stage": ns * nt,
+            "near_ties_per_stage": [int((gaps[:, :, st] < 1e-5).sum()) for st in range(g.S)],
+            "teacher_forced": o["n_forced"], "hard_mismatches": o["n_hard"],
+            "symbols_equal": bool(np.array_equal(o["symbols"], gsym)),
+            "point_mismatches": int((pts.view(np.uint64) != gpts.view(np.uint64)).any(axis=2).sum()),
+            "oracle_decode_failed_spans": int(nfail),
+            "decode_symbol_mismatches": int((dsym != gdec).sum()),
+            "lookups_checked": int(keep.sum()), "lookup_mismatches": int((lout != gout).any(axis=1).sum()),
+        })
+        sample.append("%d/%d streams x first %d/%d archived tokens" % (ns, gr["ns"], nt, cfg.T_arch))
+    tokens = cfg.batch * cfg.T_arch
+    return {"value": tokens / t_all, "unit": "archived tokens/s", "cores": threads, "kind": "oracle",
+            "cpu_model": cpu_model(),
+            "single_thread": {"value": tokens / t_one, "cores": 1,
+                              "sample": "RVQ, encode and decode on the first %d streams x first %d archived "
+                                        "tokens of each group, scaled per stream-token" % (st_streams, st_tokens)},
+            "sample": "%s of %s (full step on the sample: RVQ, encode, decode and the step's lookups that fall "
+                      "in it), time scaled per stream-token (lookups per query) to the whole workload"
+                      % ("; ".join(sample), cfg.name),
+            "checks": check}
+
+
+def gpu_checks(fkv, cfg, groups):
+    """Whole-workload checks on the GPU after the timed region: decode failures counted by the
+    kernel's own counter, round-trip symbol errors (decoded vs assigned) and lookup errors
+    (looked-up vs assigned), per group."""
+    import torch
+
+    out = []
+    for gr in groups:
+        nf = torch.zeros(1, dtype=torch.int32, device="cuda")
+        fkv.fkv_cgr_decode_spans(gr["codec"], gr["pts"], gr["n_sym"], symbols=gr["dec"], n_failed=nf)
+        fkv.fkv_span_lookup(gr["codec"], gr["pts"], gr["n_sym"], gr["g"].S, gr["qs"], gr["qt"], out=gr["out"])
+        S = gr["g"].S
+        sym = gr["sym"].view(gr["ns"], -1, S)
+        want = sym[gr["qs"].long(), gr["qt"].long()]
+        out.append({"decode_failed_spans": int(nf.item()),
+                    "roundtrip_symbol_errors": int((gr["dec"] != gr["sym"]).sum().item()),
+                    "lookup_errors": int((gr["out"] != want).any(dim=1).sum().item()),
+                    "spans": gr["ns"] * gr["n_spans"], "lookups": int(gr["qs"].numel())})
+    return out
 
 
 def reference_rates(torch):
@@ -403,11 +503,13 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="gpt2",
+    ap.add_argument("--workload", default="long_gqa",
                     choices=["gpt2", "tiny", "gpt2_hybrid_b16", "long_gqa"])
     ap.add_argument("--lookups", type=int, default=1 << 16)
-    ap.add_argument("--cpu-streams", type=int, default=288,
-                    help="streams per group the CPU oracle baseline runs on")
+    ap.add_argument("--cpu-streams", type=int, default=64,
+                    help="streams per group the CPU oracle baseline runs on (the first layer's)")
+    ap.add_argument("--cpu-tokens", type=int, default=1536,
+                    help="archived tokens per sampled stream for the CPU oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-read-stress", action="store_true",
                     help="skip the read-side measurements on the 144 x 131,072-token archive")
@@ -538,8 +640,9 @@ def main():
             r["frac_of_reference"] = round(r["achieved"] / (ref["fp16_gemm_tflops"] if r["bound"] == "mfma"
                                                             else ref["stream_gbs"]), 4)
         roof["frac_of_reference"] = rooflines[dominant]["frac_of_reference"]
+    line["gpu_checks"] = gpu_checks(fkv, cfg, groups)
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(cfg, groups, args.cpu_streams)
+        line["cpu_baseline"] = cpu_baseline(cfg, groups, args.cpu_streams, args.cpu_tokens, 8, 384)
     print(json.dumps(line), flush=True)
 
 

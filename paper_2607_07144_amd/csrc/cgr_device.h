@@ -101,14 +101,17 @@ __device__ inline int sector_fast(double qx, double qy, const uint32_t* __restri
     const float fx = (float)qx;
     const float fy = (float)qy;
     const float rs = __builtin_amdgcn_rcpf(fabsf(fx) + fabsf(fy));
-    // R = 1 - P = copysign(1 - y/(|x|+|y|), x).  |y| rs <= 1 up to rounding,
-    // so u stays within [-2^-14, 4 kLutPerUnit + 1 + 2^-14): truncation sends
-    // a slightly negative u to bucket 0, and the table repeats its last bucket
-    // in its padding; zero or non-finite input gives NaN, which converts to
-    // bucket 0.  No clamp is needed.
+    // R = 1 - P = copysign(1 - y/(|x|+|y|), x).  For a point whose |x|+|y| is
+    // a normal fp32 number, |y| rs <= 1 up to rounding, so u lies within
+    // [shift - 2^-14, 4 kLutPerUnit + 1 + 2^-14) and the table repeats its last
+    // bucket in its padding.  Other inputs occur only in corrupted points:
+    // zero gives NaN (converts to 0), a sum too small for the reciprocal gives
+    // R = +-inf (converts to INT_MIN or INT_MAX); the unsigned minimum sends
+    // every such index, and any negative one, to a padding word, so the
+    // look-up stays inside the table and the sector inside [0, N).
     const float R = __builtin_copysignf(__builtin_fmaf(-fy, rs, 1.0f), fx);
     const float u = __builtin_fmaf(R, -(float)kLutPerUnit, lut_bias);
-    const uint32_t e = lut[(int)u];
+    const uint32_t e = lut[min((uint32_t)(int)u, (uint32_t)kLutEntries)];
     // lower-edge sector (the word's low byte), plus one when the point lies
     // past the bucket's boundary: the compare sets the carry that an add with
     // byte-0 operand select consumes, so no separate mask of the low byte

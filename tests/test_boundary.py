@@ -59,27 +59,36 @@ def _fma32(a, b, c):
 LUT_BYTES = (4 * 513 + 15) // 16 * 16   # 513 bucket words, padded to 16 bytes
 
 
-def _sector_fast_emulated(tab, N, q):
+def _sector_fast_emulated(tab, N, q, flush_denormals=False):
     """NumPy emulation of the kernel's look-up-table sector search: the fp32 mirrored
     pseudo-angle R = copysign(1 - y/(|x|+|y|), x), its bucket coordinate
     u = 256 + shift - 128 R (shift puts the N-1 -> 0 boundary on a bucket edge), and the
-    bucket word (fp32 boundary fraction whose low byte holds the lower-edge sector).  u is not
-    clamped: it lies in [-2^-14, 513 + 2^-14), truncation sends a slightly negative u to
-    bucket 0, and the entries past the last bucket repeat it."""
+    bucket word (fp32 boundary fraction whose low byte holds the lower-edge sector).
+    The index follows the kernel's instructions: float-to-int conversion truncates toward zero,
+    saturates (+-inf give INT_MAX / INT_MIN) and maps NaN to 0, then an unsigned minimum with
+    513 sends any negative or oversized index to a padding word; the fraction is
+    u - floor(u) (NaN for a non-finite u, so the compare is false).  The reciprocal is exact
+    here (the hardware's is within one ulp, inside the certified margin); with
+    flush_denormals a denormal |x|+|y| is taken as zero, as a flushing reciprocal would."""
     lut = tab[16 * N:16 * N + LUT_BYTES].view("<u4")
     fx = q[:, 0].astype(np.float32)
     fy = q[:, 1].astype(np.float32)
-    rs = (np.float32(1) / (np.abs(fx) + np.abs(fy))).astype(np.float32)
-    R = np.copysign(_fma32(-fy, rs, 1.0), fx)
-    s, c = math.sin(math.pi / N), math.cos(math.pi / N)
-    u0 = c / (c + s) * 128
-    bias = np.float32(256 + (math.ceil(u0) - u0))
-    u = _fma32(R, -128.0, bias)
-    idx = u.astype(np.int32)
-    e = lut[idx]
-    frac = (u - idx.astype(np.float32)).astype(np.float32)
-    thr = e.view(np.float32)
-    return ((e & 0xFF) + (frac >= thr)).astype(np.int64)
+    with np.errstate(divide="ignore", invalid="ignore", over="ignore"):
+        den = (np.abs(fx) + np.abs(fy)).astype(np.float32)
+        if flush_denormals:
+            den = np.where(den < np.float32(2.0 ** -126), np.float32(0), den)
+        rs = (np.float32(1) / den).astype(np.float32)
+        R = np.copysign(_fma32(-fy, rs, 1.0), fx)
+        s, c = math.sin(math.pi / N), math.cos(math.pi / N)
+        u0 = c / (c + s) * 128
+        bias = np.float32(256 + (math.ceil(u0) - u0))
+        u = _fma32(R, -128.0, bias)
+        ui = np.where(np.isnan(u), 0.0, np.clip(np.trunc(u.astype(np.float64)), -2.0 ** 31, 2.0 ** 31 - 1))
+        idx = np.minimum(ui.astype(np.int64).astype(np.uint32), np.uint32(513))
+        frac = np.where(np.isfinite(u), u - np.floor(u), np.nan).astype(np.float32)
+        e = lut[idx]
+        thr = e.view(np.float32)
+        return ((e & 0xFF) + (frac >= thr)).astype(np.int64)
 
 
 @pytest.mark.parametrize("N", [3, 4, 5, 7, 16, 17, 64, 100, 256])
@@ -129,6 +138,37 @@ def test_sector_table_edges(F, orc, N):
     got = _sector_fast_emulated(tab, N, q)
     want = np.array([orc.cell(o, a, b) for a, b in q])
     assert np.array_equal(got, want), (got, want)
+
+
+@pytest.mark.parametrize("N", [3, 4, 7, 16, 64, 256])
+def test_sector_of_corrupted_points_stays_in_the_alphabet(F, N):
+    """Points no valid span reaches (zero, denormal, tiny, huge, infinite, NaN coordinates) can
+    arrive as corrupted input; their look-up index stays inside the table and their sector
+    inside [0, N), whether or not the reciprocal flushes denormals."""
+    c = F.Codec(N, 0.98)
+    tab = c.host_table()
+    vals = [0.0, -0.0, 1e-300, -1e-300, 1e-45, -1e-45, 1e-40, -3e-39, 2.0 ** -127, 1e-20, 1.0, -1.0,
+            1e30, -1e300, np.inf, -np.inf, np.nan]
+    q = np.array([(a, b) for a in vals for b in vals], dtype=np.float64)
+    for flush in (False, True):
+        got = _sector_fast_emulated(tab, N, q, flush_denormals=flush)
+        assert got.min() >= 0 and got.max() < N
+
+
+def test_sector_table_no_boundary_below_the_first_edge(F):
+    """A point at angle -pi/2 (x >= 0) has u = shift, which fp32 rounding can push up to
+    2^-14 below zero; truncation then reads bucket 0 with a fraction near 1.  That is harmless
+    when shift exceeds 2^-14 (u never goes negative) or bucket 0 holds no boundary (the carry
+    never fires); every alphabet satisfies one of the two."""
+    for N in range(3, 257):
+        c = F.Codec(N, 0.98)
+        tab = c.host_table()
+        lut = tab[16 * N:16 * N + LUT_BYTES].view("<u4")
+        s, cc = math.sin(math.pi / N), math.cos(math.pi / N)
+        u0 = cc / (cc + s) * 128
+        shift = math.ceil(u0) - u0
+        thr0 = float(np.array([lut[0] & ~np.uint32(0xFF)], np.uint32).view(np.float32)[0])
+        assert shift > 2.0 ** -14 or thr0 >= 1.0, N
 
 
 def test_invalid_arguments_are_rejected_on_the_host(F):

@@ -60,3 +60,56 @@ def test_training_lowers_distortion(fkv):
                 errs.append(float((res.double() ** 2).sum()))
             fkv.fkv_kmeans_step(xd, bd, sd, cfg.t_begin, cfg.t_end, sym, stage)
     assert errs[-1] < errs[0] and all(b <= a * 1.001 for a, b in zip(errs, errs[1:]))
+
+
+def _train(fkv, xd, bd, sd, t0, t1, iters):
+    S = bd.shape[1]
+    for it in range(iters):
+        for stage in range(S):
+            sym, _ = fkv.fkv_rvq_assign(xd, bd, sd, t0, t1)
+            fkv.fkv_kmeans_step(xd, bd, sd, t0, t1, sym, stage)
+
+
+def _trained_parity(fkv, orc, x, bd, sb, t0, t1, idx):
+    """Assignment on trained books against the oracle (teacher-forced near-ties); returns the
+    near-ties per stage and the mean of D1/||x||^2 at the last stage."""
+    xd, sd = torch.from_numpy(x).cuda(), torch.from_numpy(sb).cuda()
+    sym, res = fkv.fkv_rvq_assign(xd, bd, sd, t0, t1, want_residual=True)
+    fs, fp, fr = fkv.fkv_rvq_assign_encode(fkv.Codec(256), xd, bd, sd, t0, t1, want_residual=True)
+    assert torch.equal(fs, sym) and torch.equal(fr, res)
+    sym, res, books = host(sym), host(res), host(bd)
+    o = orc.rvq_assign(x[idx], books, sb[idx], t0, t1, force=sym[idx], force_tol=1e-5)
+    assert o["n_hard"] == 0, "index differs from the oracle outside the near-tie band on trained books"
+    assert np.array_equal(o["symbols"], sym[idx])
+    assert np.abs(o["residual"] - res[idx].astype(np.float64)).max() <= 1e-3
+    S = books.shape[1]
+    gaps = o["gaps"].reshape(len(idx), -1, S)
+    ties = [int((gaps[:, :, st] < 1e-5).sum()) for st in range(S)]
+    rel = float((o["residual"] ** 2).sum() / (x[idx][:, t0:t1].astype(np.float64) ** 2).sum())
+    return ties, rel
+
+
+def test_rvq_parity_on_trained_books_gpt2(fkv, orc):
+    """Books after 10 Lloyd iterations (Sec. 3 "Setup": codebooks trained by k-means) at the GPT-2
+    shape: the residual energy left after the stages is well below ||x||^2, which is where the
+    score offsets and the fp32 accumulation are most stressed."""
+    cfg = w.CONFIGS["gpt2"]
+    x, books, sb = w.make_group_numpy(cfg)
+    xd, bd, sd = (torch.from_numpy(a).cuda() for a in (x, books, sb))
+    _train(fkv, xd, bd, sd, cfg.t_begin, cfg.t_end, 10)
+    ties, rel = _trained_parity(fkv, orc, x, bd, sb, cfg.t_begin, cfg.t_end, np.arange(x.shape[0]))
+    print("gpt2 trained books: near-ties per stage %s, residual energy %.3f of ||x||^2" % (ties, rel))
+    assert rel < 0.9
+
+
+def test_rvq_parity_on_trained_books_long_context_heads(fkv, orc):
+    """The long-context head shape (d = 128, S = 3, K = 256, four x10 key-outlier channels) on 16
+    streams of 4,096 tokens, one book each, after 10 Lloyd iterations."""
+    cfg = w.Config(name="long_heads_sample", layers=1, heads=8, d=128, T=4096, batch=1, seed=1104,
+                   groups=(w.Group(("K", "V"), S=3, K=256, N=256),))
+    x, books, sb = w.make_group_numpy(cfg)
+    xd, bd, sd = (torch.from_numpy(a).cuda() for a in (x, books, sb))
+    _train(fkv, xd, bd, sd, cfg.t_begin, cfg.t_end, 10)
+    ties, rel = _trained_parity(fkv, orc, x, bd, sb, cfg.t_begin, cfg.t_end, np.array([0, 5, 9, 15]))
+    print("d128 trained books: near-ties per stage %s, residual energy %.3f of ||x||^2" % (ties, rel))
+    assert rel < 0.95
