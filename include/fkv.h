@@ -43,7 +43,9 @@ typedef enum {
     FKV_ERR_INVALID_ARG = -1, /* a null pointer, a size or value out of range, a bad alignment */
     FKV_ERR_UNSUPPORTED = -2, /* valid by the paper but outside what this library implements */
     FKV_ERR_LAUNCH = -3,      /* the HIP runtime refused the launch (hipGetLastError) */
-    FKV_ERR_NO_DEVICE = -4    /* no usable gfx950 device is current */
+    FKV_ERR_NO_DEVICE = -4,   /* no usable gfx950 device is current */
+    FKV_ERR_SCRATCH_TOO_SMALL = -5 /* the input needs more than the library's fixed device scratch
+                                      (allocation-free entry points only) */
 } fkv_status;
 
 /* Codec parameters of one alphabet (Sec. 1 "The code"; Fig. 1).
@@ -252,6 +254,33 @@ int fkv_kmeans_accumulate(const fkv_rvq_desc* desc, const uint16_t* x_f16, const
                           uint32_t* counts, void* stream);
 int fkv_kmeans_finalize(int32_t n_books, int32_t S, int32_t K, int32_t d, int32_t stage, const int64_t* sums,
                         const uint32_t* counts, uint16_t* books_f16, void* stream);
+
+/* ---- k-means update without allocation ------------------------------------
+ * For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  The same
+ * update as fkv_kmeans_accumulate followed by fkv_kmeans_finalize (identical
+ * books and counts, bit for bit), but the cluster sums and counts live in a
+ * device scratch array owned by the library instead of caller workspace:
+ * FKV_NOALLOC_SCRATCH_BYTES per device, held from the first call on that
+ * device until the process ends.  The call allocates and frees nothing; it
+ * clears the scratch it uses (a fill kernel, no memset) before accumulating.
+ *   desc, x_f16, stream_book, symbols, stage   as for fkv_kmeans_accumulate
+ *   books_f16   device binary16 [n_books][S][K][d], updated in place
+ *   counts_out  device u32 [n_books][K], nullable: the cluster counts
+ * Returns FKV_ERR_SCRATCH_TOO_SMALL (with no side effect) when
+ * fkv_kmeans_update_noalloc_bytes(n_books, K, d) exceeds the scratch size.
+ * Every call on one device shares that device's scratch: calls that overlap
+ * in time on one device (different streams, or several host threads) race
+ * and must be serialised by the caller. */
+#define FKV_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+/* Scratch bytes an update of n_books books of K codewords of dimension d
+ * needs: n_books*K*d*8 (sums) + n_books*K*4 (counts). */
+size_t fkv_kmeans_update_noalloc_bytes(int32_t n_books, int32_t K, int32_t d);
+
+int fkv_kmeans_update_noalloc(const fkv_rvq_desc* desc, const uint16_t* x_f16, uint16_t* books_f16,
+                              const int32_t* stream_book, const uint8_t* symbols, int32_t stage,
+                              uint32_t* counts_out, void* stream);
 
 /* Static description of a status code. */
 const char* fkv_status_string(int status);

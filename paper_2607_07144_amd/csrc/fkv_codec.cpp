@@ -147,6 +147,7 @@ extern "C" const char* fkv_status_string(int status)
     case FKV_ERR_UNSUPPORTED: return "unsupported configuration";
     case FKV_ERR_LAUNCH: return "kernel launch failed";
     case FKV_ERR_NO_DEVICE: return "no usable gfx950 device";
+    case FKV_ERR_SCRATCH_TOO_SMALL: return "input exceeds the fixed device scratch of the allocation-free entry point";
     default: return "unknown status";
     }
 }

@@ -126,6 +126,42 @@ int64_t grid_for(int64_t n)
     return b < 1 ? 1 : (b > 4096 ? 4096 : b);
 }
 
+// Zero fill of n 8-byte words (the scratch sums and counts before an update;
+// a kernel rather than a memset so that the call can be captured in a graph).
+__global__ __launch_bounds__(kThreads) void zero_words_kernel(unsigned long long* __restrict__ p, int64_t n)
+{
+    for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n; i += (int64_t)gridDim.x * kThreads) p[i] = 0;
+}
+
+// Device scratch of the allocation-free k-means update: the cluster sums
+// (int64, [n_books][K][d]) followed by the counts (u32, [n_books][K]).  Each
+// device the library runs on holds its own copy until the process ends.  In
+// host code this name is not a device address: kernels get the per-device
+// address taken once with hipGetSymbolAddress.
+static __device__ __align__(256) unsigned long long scratch[FKV_NOALLOC_SCRATCH_BYTES / 8];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices];
+
+// Address of the current device's scratch array (taken once per device);
+// nullptr when the device is unknown or the runtime refuses.
+void* scratch_address()
+{
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+            (void)hipGetLastError();
+            return nullptr;
+        }
+        g_scratch_ptr[dev] = p;
+    }
+    return g_scratch_ptr[dev];
+}
+
 }  // namespace
 }  // namespace fkv
 
@@ -173,4 +209,55 @@ extern "C" int fkv_kmeans_finalize(int32_t n_books, int32_t S, int32_t K, int32_
                        (hipStream_t)stream, (const unsigned long long*)sums, counts, (_Float16*)books_f16, d, S, K,
                        stage, n_elems);
     return launch_status();
+}
+
+extern "C" size_t fkv_kmeans_update_noalloc_bytes(int32_t n_books, int32_t K, int32_t d)
+{
+    if (n_books < 1 || K < 1 || d < 1) return 0;
+    return (size_t)n_books * K * d * 8 + (size_t)n_books * K * 4;
+}
+
+extern "C" int fkv_kmeans_update_noalloc(const fkv_rvq_desc* desc, const uint16_t* x_f16, uint16_t* books_f16,
+                                         const int32_t* stream_book, const uint8_t* symbols, int32_t stage,
+                                         uint32_t* counts_out, void* stream)
+{
+    if (!desc) return FKV_ERR_INVALID_ARG;
+    const fkv_rvq_desc& D = *desc;
+    if (D.n_streams < 0 || D.T < 0 || D.t_begin < 0 || D.t_end < D.t_begin || D.t_end > D.T) return FKV_ERR_INVALID_ARG;
+    if (D.d < 8 || D.d > 256 || D.d % 8 != 0 || D.S < 1 || D.S > 8 || D.K < 1 || D.K > 256 || D.n_books < 1)
+        return FKV_ERR_INVALID_ARG;
+    if (stage < 0 || stage >= D.S) return FKV_ERR_INVALID_ARG;
+    if (!x_f16 || !books_f16 || !stream_book || !symbols) return FKV_ERR_INVALID_ARG;
+    if (!aligned(x_f16, 16) || !aligned(books_f16, 16) || !aligned(stream_book, 4) ||
+        (counts_out && !aligned(counts_out, 4)))
+        return FKV_ERR_INVALID_ARG;
+    const size_t need = fkv_kmeans_update_noalloc_bytes(D.n_books, D.K, D.d);
+    if (need > (size_t)FKV_NOALLOC_SCRATCH_BYTES) return FKV_ERR_SCRATCH_TOO_SMALL;
+    const int64_t Ta = D.t_end - D.t_begin;
+    if (Ta * (std::min(kSlice, (int)D.d) / 8) > 0x7fffffff) return FKV_ERR_UNSUPPORTED;
+    void* base = scratch_address();
+    if (!base) return FKV_ERR_NO_DEVICE;
+    const hipStream_t st = (hipStream_t)stream;
+    unsigned long long* sums = (unsigned long long*)base;
+    const int64_t n_sum = (int64_t)D.n_books * D.K * D.d;
+    uint32_t* counts = (uint32_t*)(sums + n_sum);
+    // the previous call's contents are cleared first: sums and counts start at zero
+    const int64_t n_words = (int64_t)((need + 7) / 8);
+    hipLaunchKernelGGL(zero_words_kernel, dim3((unsigned)grid_for(n_words)), dim3(kThreads), 0, st, sums, n_words);
+    int rc = launch_status();
+    if (rc != FKV_OK) return rc;
+    if (D.n_streams > 0 && Ta > 0) {
+        rc = fkv_kmeans_accumulate(desc, x_f16, books_f16, stream_book, symbols, stage, (int64_t*)sums, counts,
+                                   stream);
+        if (rc != FKV_OK) return rc;
+    }
+    rc = fkv_kmeans_finalize(D.n_books, D.S, D.K, D.d, stage, (const int64_t*)sums, counts, books_f16, stream);
+    if (rc != FKV_OK) return rc;
+    if (counts_out) {
+        if (hipMemcpyAsync(counts_out, counts, (size_t)D.n_books * D.K * 4, hipMemcpyDeviceToDevice, st) != hipSuccess) {
+            (void)hipGetLastError();
+            return FKV_ERR_LAUNCH;
+        }
+    }
+    return FKV_OK;
 }

@@ -23,6 +23,7 @@ FKV_ERR_INVALID_ARG = -1
 FKV_ERR_UNSUPPORTED = -2
 FKV_ERR_LAUNCH = -3
 FKV_ERR_NO_DEVICE = -4
+FKV_ERR_SCRATCH_TOO_SMALL = -5
 
 
 class fkv_codec(ctypes.Structure):
@@ -56,6 +57,8 @@ _SIGS = {
     "fkv_suffix_search": ([_PC, _p, _p, _i64, _i64, _p, _i32, _i32, _p, _i64, _p, _p, _p], ctypes.c_int),
     "fkv_kmeans_accumulate": ([ctypes.POINTER(fkv_rvq_desc), _p, _p, _p, _p, _i32, _p, _p, _p], ctypes.c_int),
     "fkv_kmeans_finalize": ([_i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p], ctypes.c_int),
+    "fkv_kmeans_update_noalloc": ([ctypes.POINTER(fkv_rvq_desc), _p, _p, _p, _p, _i32, _p, _p], ctypes.c_int),
+    "fkv_kmeans_update_noalloc_bytes": ([_i32, _i32, _i32], _sz),
     "fkv_status_string": ([ctypes.c_int], ctypes.c_char_p),
     "fkv_version": ([], ctypes.c_char_p),
 }
@@ -387,6 +390,30 @@ def fkv_kmeans_step(x, books, stream_book, t_begin: int, t_end: int, symbols, st
     _check(lib.fkv_kmeans_finalize(nb, S, K, d, stage, _ptr(sums), _ptr(counts), _ptr(books), st),
            "fkv_kmeans_finalize")
     return books, counts
+
+
+def fkv_kmeans_update_noalloc(x, books, stream_book, t_begin: int, t_end: int, symbols, stage: int, counts=None,
+                              stream=None):
+    """fkv_kmeans_step without caller workspace: the cluster sums and counts live in the library's fixed
+    device scratch (no allocation in the call).  Updates `books` in place; counts int32 [n_books][K] is
+    filled when given.  Returns books."""
+    torch = _torch()
+    _need(x, torch.float16, "x")
+    _need(books, torch.float16, "books")
+    _need(stream_book, torch.int32, "stream_book")
+    _need(symbols, torch.uint8, "symbols")
+    ns, T, d = x.shape
+    nb, S, K, d2 = books.shape
+    if d2 != d or stream_book.shape != (ns,) or symbols.numel() != ns * (t_end - t_begin) * S:
+        raise ValueError("shape mismatch")
+    if counts is not None:
+        _need(counts, torch.int32, "counts")
+        if counts.numel() != nb * K:
+            raise ValueError("counts must have n_books * K entries")
+    desc = fkv_rvq_desc(ns, T, t_begin, t_end, d, S, K, nb)
+    _check(lib.fkv_kmeans_update_noalloc(ctypes.byref(desc), _ptr(x), _ptr(books), _ptr(stream_book), _ptr(symbols),
+                                         stage, _ptr(counts), _stream(stream)), "fkv_kmeans_update_noalloc")
+    return books
 
 
 def fkv_version() -> str:

@@ -326,3 +326,21 @@ def test_invalid_arguments_retrieval_kmeans_fused(F):
     assert fused(codec=F.fkv_codec(2, 6, 0.1, 0.2)) == E
     assert fused(tab=None) == E and fused(pts=None) == E and fused(pts=P(0x10008)) == E
     assert fused(D(4, 100, 4, 101, 64, 2, 256, 4)) == E
+
+
+def test_noalloc_kmeans_rejects_inputs_beyond_its_scratch(F):
+    """The allocation-free k-means update checks its inputs on the host before touching a device:
+    an input whose sums and counts exceed the fixed scratch returns FKV_ERR_SCRATCH_TOO_SMALL, and
+    the size it needs is n_books*K*d*8 + n_books*K*4 bytes."""
+    lib = F.lib
+    assert lib.fkv_kmeans_update_noalloc_bytes(288, 256, 64) == 288 * 256 * 64 * 8 + 288 * 256 * 4
+    assert lib.fkv_kmeans_update_noalloc_bytes(0, 256, 64) == 0
+    p = ctypes.c_void_p(256)   # never dereferenced: the call returns before any device work
+    big = F.fkv_rvq_desc(2048, 32768, 4, 32736, 128, 3, 256, 512)   # 134 MB of sums: beyond 64 MiB
+    assert lib.fkv_kmeans_update_noalloc(ctypes.byref(big), p, p, p, p, 0, None, None) == F.FKV_ERR_SCRATCH_TOO_SMALL
+    assert "scratch" in lib.fkv_status_string(F.FKV_ERR_SCRATCH_TOO_SMALL).decode()
+    ok = F.fkv_rvq_desc(288, 1024, 4, 992, 64, 2, 256, 288)
+    assert lib.fkv_kmeans_update_noalloc(ctypes.byref(ok), p, p, p, p, 2, None, None) == F.FKV_ERR_INVALID_ARG
+    assert lib.fkv_kmeans_update_noalloc(ctypes.byref(ok), None, p, p, p, 0, None, None) == F.FKV_ERR_INVALID_ARG
+    bad = F.fkv_rvq_desc(288, 1024, 4, 992, 60, 2, 256, 288)
+    assert lib.fkv_kmeans_update_noalloc(ctypes.byref(bad), p, p, p, p, 0, None, None) == F.FKV_ERR_INVALID_ARG
