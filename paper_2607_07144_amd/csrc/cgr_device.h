@@ -93,6 +93,18 @@ __device__ inline void encode_step(double& px, double& py, const double2 v, cons
     py = v.y + uy;
 }
 
+// The bucket word at coordinate u: the conversion to unsigned saturates
+// (negative and NaN give 0, +inf gives 2^32 - 1), and the index times four is
+// added to the table's LDS address modulo 2^32, so 2^32 - 1 lands on the
+// guard entry just before the table.  For every other input u < 516.
+__device__ __forceinline__ uint32_t lut_word(const uint32_t* lut, float u)
+{
+    uint32_t idx;
+    asm("v_cvt_u32_f32 %0, %1" : "=v"(idx) : "v"(u));
+    const uint32_t addr = (uint32_t)(uintptr_t)lut + (idx << 2);
+    return *(const __attribute__((address_space(3))) uint32_t*)(size_t)addr;
+}
+
 // Sector of a point from the pseudo-angle look-up table.  Exact for every
 // point at least kFastSectorMargin away from the sector lines (the fp32
 // pseudo-angle errs by < 1e-6 there); never leaves [0, N).
@@ -105,13 +117,12 @@ __device__ inline int sector_fast(double qx, double qy, const uint32_t* __restri
     // a normal fp32 number, |y| rs <= 1 up to rounding, so u lies within
     // [shift - 2^-14, 4 kLutPerUnit + 1 + 2^-14) and the table repeats its last
     // bucket in its padding.  Other inputs occur only in corrupted points:
-    // zero gives NaN (converts to 0), a sum too small for the reciprocal gives
-    // R = +-inf (converts to INT_MIN or INT_MAX); the unsigned minimum sends
-    // every such index, and any negative one, to a padding word, so the
-    // look-up stays inside the table and the sector inside [0, N).
+    // zero gives NaN, a sum too small for the reciprocal gives R = +-inf, and
+    // lut_word maps those to bucket 0 or the guard word, so the look-up stays
+    // inside the table and the sector inside [0, N).
     const float R = __builtin_copysignf(__builtin_fmaf(-fy, rs, 1.0f), fx);
     const float u = __builtin_fmaf(R, -(float)kLutPerUnit, lut_bias);
-    const uint32_t e = lut[min((uint32_t)(int)u, (uint32_t)kLutEntries)];
+    const uint32_t e = lut_word(lut, u);
     // lower-edge sector (the word's low byte), plus one when the point lies
     // past the bucket's boundary: the compare sets the carry that an add with
     // byte-0 operand select consumes, so no separate mask of the low byte
@@ -142,6 +153,34 @@ __device__ inline int sector_exact(double qx, double qy, const double2* __restri
         }
     }
     return best;
+}
+
+// Sectors of two independent points at once: both reciprocals, both table
+// reads, then both compares, so that one point's look-up latency overlaps the
+// other's arithmetic.  Same result as two sector_fast calls.
+__device__ inline void sector_fast2(double ax, double ay, double bx, double by, const uint32_t* __restrict__ lut,
+                                    float lut_bias, int& ca, int& cb)
+{
+    const float fxa = (float)ax, fya = (float)ay, fxb = (float)bx, fyb = (float)by;
+    const float rsa = __builtin_amdgcn_rcpf(fabsf(fxa) + fabsf(fya));
+    const float rsb = __builtin_amdgcn_rcpf(fabsf(fxb) + fabsf(fyb));
+    const float Ra = __builtin_copysignf(__builtin_fmaf(-fya, rsa, 1.0f), fxa);
+    const float Rb = __builtin_copysignf(__builtin_fmaf(-fyb, rsb, 1.0f), fxb);
+    const float ua = __builtin_fmaf(Ra, -(float)kLutPerUnit, lut_bias);
+    const float ub = __builtin_fmaf(Rb, -(float)kLutPerUnit, lut_bias);
+    const uint32_t ea = lut_word(lut, ua);
+    const uint32_t eb = lut_word(lut, ub);
+    const float fa = __builtin_amdgcn_fractf(ua), fb = __builtin_amdgcn_fractf(ub);
+    uint32_t xa, xb;
+    asm("v_cmp_ge_f32 vcc, %2, %3\n\t"
+        "v_addc_co_u32_sdwa %0, vcc, %6, %3, vcc dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_0\n\t"
+        "v_cmp_ge_f32 vcc, %4, %5\n\t"
+        "v_addc_co_u32_sdwa %1, vcc, %6, %5, vcc dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_0"
+        : "=&v"(xa), "=&v"(xb)
+        : "v"(fa), "v"(ea), "v"(fb), "v"(eb), "v"(0u)
+        : "vcc");
+    ca = (int)xa;
+    cb = (int)xb;
 }
 
 template <bool EXACT>

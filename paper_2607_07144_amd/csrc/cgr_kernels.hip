@@ -69,9 +69,35 @@ __global__ __launch_bounds__(kBlock, 8) void cgr_encode_tiles_kernel(
 }
 
 // Span encode for spans of up to 16 symbols, with no LDS staging: a wave
-// takes 64 consecutive spans of one stream (a wave tile), each lane loads the
-// two to five aligned dwords that cover its span, extracts the symbols and
-// walks them from the anchor.  Wave tiles are walked without division.
+// takes 128 consecutive spans of one stream (a wave tile), two per lane (j and
+// j + 64), loads the aligned dwords that cover each span, extracts the symbols
+// and walks both spans from the anchor as two independent chains.  Wave tiles
+// are walked without division.
+constexpr int kEncSpl = 4;
+constexpr int kEncTile = 64 * kEncSpl;
+
+__device__ __forceinline__ void span_dwords(const uint8_t* __restrict__ sym, const uint32_t* __restrict__ s32,
+                                            int64_t a, int len, int64_t n_dw, int64_t total_bytes, uint32_t (&e)[4])
+{
+    const int off = (int)(a & 3);
+    const int64_t d0 = a >> 2;
+    uint32_t dw[5];
+#pragma unroll
+    for (int q = 0; q < 5; ++q) {
+        const int64_t d = d0 + q;
+        dw[q] = 0;
+        if (q * 4 < off + len) {
+            if (d < n_dw) {
+                dw[q] = s32[d];
+            } else {   // the array's last, partial dword, byte by byte
+                for (int b = 0; b < 4 && d * 4 + b < total_bytes; ++b) dw[q] |= (uint32_t)sym[d * 4 + b] << (8 * b);
+            }
+        }
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) e[c] = __builtin_amdgcn_alignbyte(dw[c + 1], dw[c], off);
+}
+
 __global__ __launch_bounds__(kBlock, 8) void cgr_encode_kernel(
     const uint8_t* __restrict__ sym, double2* __restrict__ pts, const uint8_t* __restrict__ gtab,
     CodecArgs cd, int64_t n_sym, int64_t n_spans, int64_t wtiles_per_stream, int64_t n_wtiles, int64_t total_bytes)
@@ -90,33 +116,27 @@ __global__ __launch_bounds__(kBlock, 8) void cgr_encode_kernel(
     TileWalk w;
     w.init(wave, n_waves, wtiles_per_stream);
     for (int64_t t = wave; t < n_wtiles; t += n_waves, w.next()) {
-        const int64_t j = w.j * 64 + lane;
-        if (j >= n_spans) continue;
-        const int64_t a = w.s * n_sym + j * L;
-        const int len = (int)min((int64_t)L, n_sym - j * L);
-        const int off = (int)(a & 3);
-        const int64_t d0 = a >> 2;
-        uint32_t dw[5];
+        int64_t jj[kEncSpl];
+        int len[kEncSpl];
+        uint32_t e[kEncSpl][4];
 #pragma unroll
-        for (int q = 0; q < 5; ++q) {
-            const int64_t d = d0 + q;
-            dw[q] = 0;
-            if (q * 4 < off + len) {
-                if (d < n_dw) {
-                    dw[q] = s32[d];
-                } else {   // the array's last, partial dword, byte by byte
-                    for (int b = 0; b < 4 && d * 4 + b < total_bytes; ++b) dw[q] |= (uint32_t)sym[d * 4 + b] << (8 * b);
-                }
-            }
+        for (int h = 0; h < kEncSpl; ++h) {
+            jj[h] = w.j * kEncTile + h * 64 + lane;
+            len[h] = jj[h] < n_spans ? (int)min((int64_t)L, n_sym - jj[h] * L) : 0;
+            e[h][0] = e[h][1] = e[h][2] = e[h][3] = 0;
+            if (len[h] > 0) span_dwords(sym, s32, w.s * n_sym + jj[h] * L, len[h], n_dw, total_bytes, e[h]);
         }
-        uint32_t e[4];   // symbols 4c..4c+3 of the span
+        double px[kEncSpl], py[kEncSpl];
 #pragma unroll
-        for (int c = 0; c < 4; ++c) e[c] = __builtin_amdgcn_alignbyte(dw[c + 1], dw[c], off);
-        double px = 0.0, py = 0.0;
+        for (int h = 0; h < kEncSpl; ++h) px[h] = py[h] = 0.0;
 #pragma unroll
         for (int k = 0; k < 16; ++k)
-            if (k < len) encode_step(px, py, V[(e[k >> 2] >> (8 * (k & 3))) & 0xFF], cd.r);
-        pts[w.s * n_spans + j] = make_double2(px, py);
+#pragma unroll
+            for (int h = 0; h < kEncSpl; ++h)
+                if (k < len[h]) encode_step(px[h], py[h], V[(e[h][k >> 2] >> (8 * (k & 3))) & 0xFF], cd.r);
+#pragma unroll
+        for (int h = 0; h < kEncSpl; ++h)
+            if (len[h] > 0) pts[w.s * n_spans + jj[h]] = make_double2(px[h], py[h]);
     }
 }
 
@@ -154,12 +174,18 @@ __device__ __forceinline__ void walk_two(double& ax, double& ay, double& bx, dou
     const int n = LC > 0 ? LC : len;
 #pragma unroll
     for (int k = n - 1; k >= 0; --k) {
-        const int ca = sector_of<EXACT>(ax, ay, t, cd);
-        const int cb = sector_of<EXACT>(bx, by, t, cd);
+        int ca, cb;
+        if (EXACT) {
+            ca = sector_of<EXACT>(ax, ay, t, cd);
+            cb = sector_of<EXACT>(bx, by, t, cd);
+        } else {
+            sector_fast2(ax, ay, bx, by, t.lut, cd.lut_bias, ca, cb);
+        }
         my0[k] = (uint8_t)ca;
         my1[k] = (uint8_t)cb;
-        decode_step(ax, ay, t.Wr[ca], cd.inv_r);
-        decode_step(bx, by, t.Wr[cb], cd.inv_r);
+        const double2 wa = t.Wr[ca], wb = t.Wr[cb];
+        decode_step(ax, ay, wa, cd.inv_r);
+        decode_step(bx, by, wb, cd.inv_r);
     }
 }
 
@@ -307,7 +333,7 @@ extern "C" int fkv_cgr_encode_spans(const fkv_codec* c, const void* dev_table, c
         return FKV_ERR_INVALID_ARG;
     const int64_t n_spans = (n_sym + c->L - 1) / c->L;
     if (c->L <= 16) {
-        const int64_t wtps = (n_spans + 63) / 64;
+        const int64_t wtps = (n_spans + kEncTile - 1) / kEncTile;
         const int64_t n_wtiles = wtps * n_streams;
         const int64_t nb = min((int64_t)kMaxBlocks, (n_wtiles + kBlock / 64 - 1) / (kBlock / 64));
         hipLaunchKernelGGL(cgr_encode_kernel, dim3((unsigned)nb), dim3(kBlock), 0, (hipStream_t)stream, symbols,

@@ -135,7 +135,13 @@ extern "C" int fkv_codec_fill_table(const fkv_codec* c, void* host_table)
     // the section's padding repeats the last bucket: a coordinate that rounds
     // just past the range's upper end (the direction -pi/2 approached with
     // x < 0) reads the bucket it belongs to, with no clamp in the kernels
-    for (size_t i = fkv::kLutEntries; i < fkv::kLutBytes / sizeof(uint32_t); ++i) lut[i] = lut[fkv::kLutEntries - 1];
+    for (size_t i = fkv::kLutEntries; i < (fkv::kLutBytes - fkv::kLutGuard) / sizeof(uint32_t); ++i)
+        lut[i] = lut[fkv::kLutEntries - 1];
+    // the guard entries before the table: sector 0, no boundary (threshold 2)
+    const float two = 2.0f;
+    uint32_t gw;
+    memcpy(&gw, &two, sizeof gw);
+    for (size_t i = 1; i <= fkv::kLutGuard / sizeof(uint32_t); ++i) lut[-(ptrdiff_t)i] = gw & ~0xFFu;
     return FKV_OK;
 }
 

@@ -28,8 +28,11 @@ namespace fkv {
 // = 2 kLutPerUnit + shift - R kLutPerUnit, in [0, 4 kLutPerUnit + 1).
 constexpr int kLutPerUnit = 128;
 constexpr int kLutEntries = 4 * kLutPerUnit + 1;
-constexpr size_t kLutBytes = (sizeof(uint32_t) * kLutEntries + 15) / 16 * 16;
-static_assert(kLutBytes / sizeof(uint32_t) >= kLutEntries + 1, "the look-up table needs a padding entry");
+// The section: 16 bytes whose last word is a guard entry (sector 0, no
+// boundary) right before the table, then the entries, padded to 16 bytes.
+constexpr size_t kLutGuard = 16;
+constexpr size_t kLutBytes = kLutGuard + (sizeof(uint32_t) * kLutEntries + 15) / 16 * 16;
+static_assert((kLutBytes - kLutGuard) / sizeof(uint32_t) >= kLutEntries + 1, "the look-up table needs a padding entry");
 
 // (P + 1) kLutPerUnit of the wrap boundary is c/(c+s) kLutPerUnit with
 // c = cos(pi/N), s = sin(pi/N); the shift lifts it to the next integer.
@@ -43,12 +46,13 @@ inline double lut_shift(int N)
 // Device table, one per alphabet, 16-byte aligned sections, ordered so that
 // the inverse map's fast path needs only the first two:
 //   [0,             16N)            Wr[c] = W[c] / r                double2
-//   [16N,           16N + B)        sector look-up table            uint32_t[513]
+//   [16N,           16N + B)        16 bytes ending in a guard word, then the
+//                                   sector look-up table            uint32_t[513]
 //   [16N + B,       32N + B)        V[c]  = (cos 2 pi c/N, sin 2 pi c/N)
 //   [32N + B,       48N + B)        W[c]  = (1 - r) V[c]  (cell centres)
 // with B = kLutBytes.
 constexpr size_t table_off_Wr(int) { return 0; }
-constexpr size_t table_off_lut(int N) { return (size_t)16 * N; }
+constexpr size_t table_off_lut(int N) { return (size_t)16 * N + kLutGuard; }
 constexpr size_t table_off_V(int N) { return (size_t)16 * N + kLutBytes; }
 constexpr size_t table_off_W(int N) { return (size_t)32 * N + kLutBytes; }
 constexpr size_t table_bytes(int N) { return (size_t)48 * N + kLutBytes; }

@@ -12,7 +12,7 @@ import pytest
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "fkv.h")
 # bytes of the decode look-up table inside the codec's device table (513 words, 16-byte padded)
-LUT_BYTES = 2064
+LUT_BYTES = 2080   # sector-table section: a 16-byte guard block, then 513 words padded to 16 bytes
 
 
 @pytest.fixture(scope="module")
@@ -56,7 +56,8 @@ def _fma32(a, b, c):
     return (np.asarray(a, np.float64) * np.asarray(b, np.float64) + np.float64(c)).astype(np.float32)
 
 
-LUT_BYTES = (4 * 513 + 15) // 16 * 16   # 513 bucket words, padded to 16 bytes
+LUT_GUARD = 16                            # guard block before the bucket words (its last word: sector 0)
+LUT_WORDS = (4 * 513 + 15) // 16 * 4      # 513 bucket words, padded to 16 bytes
 
 
 def _sector_fast_emulated(tab, N, q, flush_denormals=False):
@@ -64,13 +65,15 @@ def _sector_fast_emulated(tab, N, q, flush_denormals=False):
     pseudo-angle R = copysign(1 - y/(|x|+|y|), x), its bucket coordinate
     u = 256 + shift - 128 R (shift puts the N-1 -> 0 boundary on a bucket edge), and the
     bucket word (fp32 boundary fraction whose low byte holds the lower-edge sector).
-    The index follows the kernel's instructions: float-to-int conversion truncates toward zero,
-    saturates (+-inf give INT_MAX / INT_MIN) and maps NaN to 0, then an unsigned minimum with
-    513 sends any negative or oversized index to a padding word; the fraction is
-    u - floor(u) (NaN for a non-finite u, so the compare is false).  The reciprocal is exact
-    here (the hardware's is within one ulp, inside the certified margin); with
-    flush_denormals a denormal |x|+|y| is taken as zero, as a flushing reciprocal would."""
-    lut = tab[16 * N:16 * N + LUT_BYTES].view("<u4")
+    The index follows the kernel's instructions: the float-to-unsigned conversion truncates toward
+    zero and saturates (negative values and NaN give 0, +inf and values beyond 2^32 - 1 give
+    2^32 - 1), and index 2^32 - 1 reads, through the wrapping 32-bit LDS address, the guard word
+    just before the table (sector 0, no boundary); the fraction is u - floor(u) (NaN for a
+    non-finite u, so the compare is false).  The reciprocal is exact here (the hardware's is within
+    one ulp, inside the certified margin); with flush_denormals a denormal |x|+|y| is taken as zero,
+    as a flushing reciprocal would."""
+    guard = tab[16 * N:16 * N + LUT_GUARD].view("<u4")[-1]
+    lut = tab[16 * N + LUT_GUARD:16 * N + LUT_GUARD + 4 * LUT_WORDS].view("<u4")
     fx = q[:, 0].astype(np.float32)
     fy = q[:, 1].astype(np.float32)
     with np.errstate(divide="ignore", invalid="ignore", over="ignore"):
@@ -83,10 +86,11 @@ def _sector_fast_emulated(tab, N, q, flush_denormals=False):
         u0 = c / (c + s) * 128
         bias = np.float32(256 + (math.ceil(u0) - u0))
         u = _fma32(R, -128.0, bias)
-        ui = np.where(np.isnan(u), 0.0, np.clip(np.trunc(u.astype(np.float64)), -2.0 ** 31, 2.0 ** 31 - 1))
-        idx = np.minimum(ui.astype(np.int64).astype(np.uint32), np.uint32(513))
+        ui = np.where(np.isnan(u), 0.0, np.clip(np.trunc(u.astype(np.float64)), 0.0, 2.0 ** 32 - 1))
+        idx = ui.astype(np.int64)
         frac = np.where(np.isfinite(u), u - np.floor(u), np.nan).astype(np.float32)
-        e = lut[idx]
+        assert np.all((idx < LUT_WORDS) | (idx == 2 ** 32 - 1)), "bucket index outside the table"
+        e = np.where(idx == 2 ** 32 - 1, guard, lut[np.minimum(idx, LUT_WORDS - 1)]).astype(np.uint32)
         thr = e.view(np.float32)
         return ((e & 0xFF) + (frac >= thr)).astype(np.int64)
 
@@ -124,13 +128,16 @@ def test_sector_table_agrees_with_oracle_cells(F, orc, N):
 @pytest.mark.parametrize("N", [4, 8, 16, 64, 256])
 def test_sector_table_edges(F, orc, N):
     """The ends of the bucket range: points on the axes (R = +-1, 0 and +-2, including a signed
-    zero x, which selects the first or the last bucket) give the oracle's cell, and the table's
-    padding words repeat its last bucket, so the unclamped bucket index stays inside the table."""
+    zero x, which selects the first or the last bucket) give the oracle's cell, the table's
+    padding words repeat its last bucket, and the guard words before it hold sector 0 with no
+    boundary, so the unclamped bucket index always reads a word of the section."""
     c = F.Codec(N, 0.98)
     o = orc.Codec(N, 0.98)
     tab = c.host_table()
-    lut = tab[16 * N:16 * N + LUT_BYTES].view("<u4")
+    lut = tab[16 * N + LUT_GUARD:16 * N + LUT_GUARD + 4 * LUT_WORDS].view("<u4")
     assert np.all(lut[513:] == lut[512])
+    guard = tab[16 * N:16 * N + LUT_GUARD].view("<u4")
+    assert np.all(guard & 0xFF == 0) and np.all((guard & ~np.uint32(0xFF)).view(np.float32) == 2.0)
     pts = []
     for a in (1e-3, 0.25, 0.5, 1.0):
         pts += [(a, 0.0), (-a, 0.0), (0.0, a), (0.0, -a), (-0.0, -a), (-0.0, a)]
@@ -163,7 +170,7 @@ def test_sector_table_no_boundary_below_the_first_edge(F):
     for N in range(3, 257):
         c = F.Codec(N, 0.98)
         tab = c.host_table()
-        lut = tab[16 * N:16 * N + LUT_BYTES].view("<u4")
+        lut = tab[16 * N + LUT_GUARD:16 * N + LUT_GUARD + 4 * LUT_WORDS].view("<u4")
         s, cc = math.sin(math.pi / N), math.cos(math.pi / N)
         u0 = cc / (cc + s) * 128
         shift = math.ceil(u0) - u0
