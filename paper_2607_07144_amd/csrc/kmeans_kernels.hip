@@ -30,6 +30,7 @@ constexpr int kThreads = 256;
 // walked in 1024-task steps, each task waiting on its symbol, row and earlier
 // codewords).
 constexpr int kAccThreads = 1024;
+constexpr int kAccBatch = 4;   // tasks per thread whose loads are in flight together
 
 // One block per (book, 64-dimension slice): the block owns that slice of the
 // book's cluster sums, accumulates every member token of every stream of the
@@ -69,28 +70,65 @@ __global__ __launch_bounds__(kAccThreads) void kmeans_accumulate_kernel(
         const int nm = *n_match;
         for (int m = 0; m < nm; ++m) {
             const int64_t s = s0 + match[m];
-            // 32-bit task walk (the host checks that Ta * nch fits)
+            // 32-bit task walk (the host checks that Ta * nch fits).  Each thread
+            // takes kAccBatch tasks at a time and issues all their loads before
+            // any sum, so the latencies of the batch overlap.
             const int n_task = (int)(Ta * nch);
-            for (int task = threadIdx.x; task < n_task; task += kAccThreads) {
-                const int t = task / nch;
-                const int ch = task - t * nch;
-                const uint8_t* sym = symbols + (s * Ta + t) * S;
-                bool bad = false;
-                for (int st = 0; st <= stage; ++st) bad = bad || sym[st] >= K;
-                if (bad) continue;   // a symbol outside the book: the token is skipped
-                const half8 xv = *(const half8*)(x + (s * T + t_begin + t) * d + e0 + ch * 8);
-                double r[8];
+            for (int task0 = threadIdx.x; task0 < n_task; task0 += kAccThreads * kAccBatch) {
+                int cl[kAccBatch];          // cluster of each task, -1: none (past the end, or skipped)
+                int64_t row[kAccBatch];     // token row of x
+                const uint8_t* sym[kAccBatch];
+                int chn[kAccBatch];
 #pragma unroll
-                for (int e = 0; e < 8; ++e) r[e] = (double)xv[e];
-                for (int st = 0; st < stage; ++st) {
-                    const half8 c = *(const half8*)(books + (((int64_t)b * S + st) * K + sym[st]) * d + e0 + ch * 8);
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) r[e] = r[e] - (double)c[e];
+                for (int u = 0; u < kAccBatch; ++u) {
+                    const int task = task0 + u * kAccThreads;
+                    const int t = task / nch;
+                    chn[u] = task - t * nch;
+                    sym[u] = symbols + (s * Ta + (task < n_task ? t : 0)) * S;
+                    row[u] = s * T + t_begin + (task < n_task ? t : 0);
+                    cl[u] = task < n_task ? 0 : -1;
                 }
-                unsigned long long* dst = ls + (size_t)sym[stage] * pitch + ch * 8;
+                uint64_t sy[kAccBatch];     // the task's symbols of stages 0..stage, one byte each
 #pragma unroll
-                for (int e = 0; e < 8; ++e) atomicAdd(dst + e, (unsigned long long)(long long)ldexp(r[e], 24));
-                if (ch == 0 && slice == 0) atomicAdd(lc + sym[stage], 1u);
+                for (int u = 0; u < kAccBatch; ++u) {
+                    sy[u] = 0;
+                    for (int st = 0; st <= stage; ++st) sy[u] |= (uint64_t)sym[u][st] << (8 * st);
+                }
+                half8 xv[kAccBatch];
+#pragma unroll
+                for (int u = 0; u < kAccBatch; ++u) xv[u] = *(const half8*)(x + row[u] * d + e0 + chn[u] * 8);
+#pragma unroll
+                for (int u = 0; u < kAccBatch; ++u) {
+                    bool bad = cl[u] < 0;
+                    for (int st = 0; st <= stage; ++st) bad = bad || (int)((sy[u] >> (8 * st)) & 255u) >= K;
+                    cl[u] = bad ? -1 : (int)((sy[u] >> (8 * stage)) & 255u);   // outside the book: skipped
+                }
+                double r[kAccBatch][8];
+#pragma unroll
+                for (int u = 0; u < kAccBatch; ++u)
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) r[u][e] = (double)xv[u][e];
+                for (int st = 0; st < stage; ++st) {
+                    half8 c[kAccBatch];
+#pragma unroll
+                    for (int u = 0; u < kAccBatch; ++u)
+                        c[u] = *(const half8*)(books +
+                                               (((int64_t)b * S + st) * K + (cl[u] < 0 ? 0 : (int)((sy[u] >> (8 * st)) & 255u))) * d +
+                                               e0 + chn[u] * 8);
+#pragma unroll
+                    for (int u = 0; u < kAccBatch; ++u)
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) r[u][e] = r[u][e] - (double)c[u][e];
+                }
+#pragma unroll
+                for (int u = 0; u < kAccBatch; ++u) {
+                    if (cl[u] < 0) continue;
+                    unsigned long long* dst = ls + (size_t)cl[u] * pitch + chn[u] * 8;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        atomicAdd(dst + e, (unsigned long long)(long long)ldexp(r[u][e], 24));
+                    if (chn[u] == 0 && slice == 0) atomicAdd(lc + cl[u], 1u);
+                }
             }
         }
         __syncthreads();   // the list is rewritten for the next chunk
@@ -184,7 +222,7 @@ extern "C" int fkv_kmeans_accumulate(const fkv_rvq_desc* desc, const uint16_t* x
         !aligned(stream_book, 4))
         return FKV_ERR_INVALID_ARG;
     const int n_slices = (D.d + kSlice - 1) / kSlice;
-    if (Ta * (std::min(kSlice, (int)D.d) / 8) > 0x7fffffff) return FKV_ERR_UNSUPPORTED;
+    if (Ta * (std::min(kSlice, (int)D.d) / 8) > 0x7fffffff - kAccThreads * kAccBatch) return FKV_ERR_UNSUPPORTED;
     const size_t shm = (size_t)D.K * (std::min(kSlice, (int)D.d) + 1) * 8 + (size_t)D.K * 4 + (kAccThreads + 1) * 4;
     static std::once_flag once;
     std::call_once(once, [] {
@@ -234,7 +272,7 @@ extern "C" int fkv_kmeans_update_noalloc(const fkv_rvq_desc* desc, const uint16_
     const size_t need = fkv_kmeans_update_noalloc_bytes(D.n_books, D.K, D.d);
     if (need > (size_t)FKV_NOALLOC_SCRATCH_BYTES) return FKV_ERR_SCRATCH_TOO_SMALL;
     const int64_t Ta = D.t_end - D.t_begin;
-    if (Ta * (std::min(kSlice, (int)D.d) / 8) > 0x7fffffff) return FKV_ERR_UNSUPPORTED;
+    if (Ta * (std::min(kSlice, (int)D.d) / 8) > 0x7fffffff - kAccThreads * kAccBatch) return FKV_ERR_UNSUPPORTED;
     void* base = scratch_address();
     if (!base) return FKV_ERR_NO_DEVICE;
     const hipStream_t st = (hipStream_t)stream;
