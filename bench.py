@@ -11,7 +11,9 @@ one).  Inputs are resident in device memory before the timed region.
 Prints one JSON line.  `value` is archived tokens per second over the whole
 step (a token is one position across all layers, heads and K/V); per-phase
 rates, the dominant kernel's roofline fraction and the CPU oracle's rate on the
-same workload are reported beside it.  The step is captured once as a HIP graph
+same workload are reported beside it.  `other_workloads` gives the GPT-2-shaped
+and hybrid workloads' step rate and, per group, the fused kernel against the
+matrix peak and HBM and the bulk decode against HBM.  The step is captured once as a HIP graph
 and replayed (no host launch overhead in the timed region); each kernel's
 average duration comes from a graph of back-to-back launches of that kernel.
 `reference_rates` gives what a library fp16 GEMM and a streaming elementwise
@@ -174,6 +176,47 @@ def time_graph(fn, reps: int, replays: int, stream):
     e1.record()
     torch.cuda.synchronize()
     return e0.elapsed_time(e1) / 1e3 / (reps * replays)
+
+
+def other_workloads(fkv, side, names, n_lookups: int, steps: int, warmup: int):
+    """The GPT-2-shaped and hybrid workloads measured the same way as the headline one, per group:
+    the fused assignment + encode launch against the matrix peak and against HBM (the hybrid
+    value group is HBM-bound), bulk decode against HBM, and the whole step as archived tokens/s."""
+    import torch
+
+    out = {}
+    for name in names:
+        cfg, groups = build_workload(name, n_lookups)
+        with torch.cuda.stream(side):
+            for _ in range(max(1, warmup)):
+                run_step(fkv, cfg, groups)
+        torch.cuda.synchronize()
+        step_s = time_graph(lambda: run_step(fkv, cfg, groups), 1, max(1, steps), side)
+        per_group = []
+        for gr in groups:
+            g, ns, d = gr["g"], gr["ns"], cfg.d
+            nb = gr["books"].shape[0]
+            flops = ns * cfg.T_arch * g.S * 2 * g.K * d
+            fused_bytes = (ns * cfg.T_arch * d * 2 + nb * g.S * g.K * d * 2 + ns * gr["n_sym"] +
+                           ns * gr["n_spans"] * 16)
+            codec_bytes = ns * gr["n_sym"] + ns * gr["n_spans"] * 16
+            t_f = time_graph(lambda: run_kernel(fkv, cfg, [gr], "rvq_assign_encode"), 10, max(1, steps // 4), side)
+            t_d = time_graph(lambda: run_kernel(fkv, cfg, [gr], "cgr_decode"), 10, max(1, steps // 4), side)
+            per_group.append({
+                "kinds": list(g.kinds), "S": g.S, "K": g.K, "N": g.N, "L": gr["codec"].L, "streams": ns,
+                "rvq_assign_encode": {"avg_launch_us": round(t_f * 1e6, 2),
+                                      "tflops": round(flops / t_f / 1e12, 2),
+                                      "mfma_frac": round(flops / t_f / 1e12 / PEAK_FP16_MFMA_TFLOPS, 4),
+                                      "gbs": round(fused_bytes / t_f / 1e9, 1),
+                                      "hbm_frac": round(fused_bytes / t_f / 1e9 / PEAK_HBM_GBS, 4)},
+                "cgr_decode": {"avg_launch_us": round(t_d * 1e6, 2), "gbs": round(codec_bytes / t_d / 1e9, 1),
+                               "hbm_frac": round(codec_bytes / t_d / 1e9 / PEAK_HBM_GBS, 4)},
+            })
+        out[name] = {"description": cfg.description, "archived_tokens_per_s": round(cfg.batch * cfg.T_arch / step_s, 1),
+                     "ms_per_step": round(step_s * 1e3, 5), "groups": per_group}
+        del groups
+        torch.cuda.empty_cache()
+    return out
 
 
 def next_rows(fkv, cfg, groups, side, replays: int):
@@ -513,6 +556,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-read-stress", action="store_true",
                     help="skip the read-side measurements on the 144 x 131,072-token archive")
+    ap.add_argument("--no-other-workloads", action="store_true",
+                    help="skip the GPT-2-shaped and hybrid workloads measured beside the headline one")
     ap.add_argument("--no-reference-rates", action="store_true",
                     help="skip the library GEMM and streaming-kernel reference rates")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -581,6 +626,10 @@ def main():
     extra = next_rows(fkv, cfg, groups, side, max(1, args.steps // 4))
     if not args.no_read_stress:
         extra["read_stress"] = read_stress(fkv, side, max(1, args.steps // 4))
+    others_res = None
+    if not args.no_other_workloads:
+        others = [n for n in ("gpt2", "gpt2_hybrid_b16") if n != cfg.name]
+        others_res = other_workloads(fkv, side, others, args.lookups, args.steps, args.warmup)
     alg = algorithmic(cfg, groups)
     tokens = cfg.batch * cfg.T_arch
     launches = len(groups)
@@ -628,6 +677,7 @@ def main():
         "roofline": roof,
         "rooflines": rooflines,
         "next_rows": extra,
+        "other_workloads": others_res,
         "reference_rates": None,
         "cpu_baseline": None,
     }
