@@ -178,10 +178,12 @@ def time_graph(fn, reps: int, replays: int, stream):
     return e0.elapsed_time(e1) / 1e3 / (reps * replays)
 
 
-def other_workloads(fkv, side, names, n_lookups: int, steps: int, warmup: int):
+def other_workloads(fkv, side, names, n_lookups: int, steps: int, warmup: int, cpu: bool):
     """The GPT-2-shaped and hybrid workloads measured the same way as the headline one, per group:
     the fused assignment + encode launch against the matrix peak and against HBM (the hybrid
-    value group is HBM-bound), bulk decode against HBM, and the whole step as archived tokens/s."""
+    value group is HBM-bound), bulk decode against HBM, and the whole step as archived tokens/s.
+    With `cpu`, the oracle is timed and checks the GPU on the GPT-2 shape in full and on the first
+    64 streams of each hybrid group."""
     import torch
 
     out = {}
@@ -214,6 +216,9 @@ def other_workloads(fkv, side, names, n_lookups: int, steps: int, warmup: int):
             })
         out[name] = {"description": cfg.description, "archived_tokens_per_s": round(cfg.batch * cfg.T_arch / step_s, 1),
                      "ms_per_step": round(step_s * 1e3, 5), "groups": per_group}
+        if cpu:
+            out[name]["cpu_oracle"] = cpu_baseline(cfg, groups, max(gr["ns"] for gr in groups) if name == "gpt2" else 64,
+                                                   cfg.T_arch, 8, 384)
         del groups
         torch.cuda.empty_cache()
     return out
@@ -629,7 +634,8 @@ def main():
     others_res = None
     if not args.no_other_workloads:
         others = [n for n in ("gpt2", "gpt2_hybrid_b16") if n != cfg.name]
-        others_res = other_workloads(fkv, side, others, args.lookups, args.steps, args.warmup)
+        others_res = other_workloads(fkv, side, others, args.lookups, args.steps, args.warmup,
+                                     not args.no_cpu_baseline)
     alg = algorithmic(cfg, groups)
     tokens = cfg.batch * cfg.T_arch
     launches = len(groups)
