@@ -288,7 +288,7 @@ def next_rows(fkv, cfg, groups, side, replays: int):
     }
 
 
-def read_stress(fkv, side, replays: int):
+def read_stress(fkv, side, replays: int, cpu: bool = False):
     """Read side at HBM scale: the 144-stream x 131,072-token archive (2 symbols per token, N = 256).
     Bulk decode rotates over 4 copies of the points so that consecutive launches do not hit the
     memory-side cache; 2^20 random lookups, beside a library gather of the same queries' points (the
@@ -341,8 +341,42 @@ def read_stress(fkv, side, replays: int):
     lk_bytes = int(qs_h.size * (8 + c["S"]) + 16 * ((a + c["S"] - 1) // L - a // L + 1).sum())
     hbm = lambda b, t: {"bound": "hbm", "achieved": round(b / t / 1e9, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                         "frac": round(b / t / 1e9 / PEAK_HBM_GBS, 4)}
+    cpu_res = None
+    if cpu:
+        # the oracle on this host: encode and bulk decode of the first 16 streams, and the first
+        # 65,536 queries, each scaled to the whole archive / all queries; and as checker of the
+        # GPU's points, decoded symbols and lookups there
+        import oracle
+
+        threads = oracle.default_threads()
+        oc = oracle.Codec(c["N"])
+        n_s = 16
+        t0 = time.perf_counter()
+        opts = oracle.encode(oc, sym_h[:n_s], threads=threads)
+        t1 = time.perf_counter()
+        odec, _, onf, _ = oracle.decode(oc, opts, n_sym, threads=threads)
+        t2 = time.perf_counter()
+        nq = 1 << 16
+        oq = qs_h[:nq].astype(np.uint32), qt_h[:nq].astype(np.uint32)
+        lpts = pts.cpu().numpy()
+        t3 = time.perf_counter()
+        lout, lst, _ = oracle.lookup(oc, lpts, n_sym, c["S"], oq[0], oq[1], threads=threads)
+        t4 = time.perf_counter()
+        gpts = pts[:n_s].cpu().numpy()
+        cpu_res = {"cores": threads, "cpu_model": cpu_model(), "kind": "oracle",
+                   "sample": "encode and bulk decode of the first %d of %d streams, lookups of the first %d of %d "
+                             "queries, scaled to the whole archive" % (n_s, ns, nq, qs_h.size),
+                   "encode_symbols_per_s": round(n_s * n_sym / (t1 - t0), 1),
+                   "decode_symbols_per_s": round(n_s * n_sym / (t2 - t1), 1),
+                   "lookups_per_s": round(nq / (t4 - t3), 1),
+                   "checks": {"point_mismatches": int((opts.view(np.uint64) != gpts.view(np.uint64)).any(axis=2).sum()),
+                              "oracle_decode_failed_spans": int(onf),
+                              "decode_symbol_mismatches": int((odec != dec[:n_s].cpu().numpy()).sum()),
+                              "lookup_mismatches": int((lout != out[:nq].cpu().numpy()).any(axis=1).sum()),
+                              "lookup_status_nonzero": int((lst != 0).sum())}}
     return {
         "archive": "%d streams x %d symbols, N=%d, L=%d" % (ns, n_sym, c["N"], L),
+        "cpu_oracle": cpu_res,
         "bulk_decode": {"avg_launch_us": round(t_dec * 1e6, 2), "symbols_per_s": round(n_pos / t_dec, 1),
                         "roofline": hbm(dec_bytes, t_dec), "rotation": 4, "decode_failed_spans": int(nf.item()),
                         "roundtrip_symbol_errors": dec_err},
@@ -630,7 +664,7 @@ def main():
 
     extra = next_rows(fkv, cfg, groups, side, max(1, args.steps // 4))
     if not args.no_read_stress:
-        extra["read_stress"] = read_stress(fkv, side, max(1, args.steps // 4))
+        extra["read_stress"] = read_stress(fkv, side, max(1, args.steps // 4), not args.no_cpu_baseline)
     others_res = None
     if not args.no_other_workloads:
         others = [n for n in ("gpt2", "gpt2_hybrid_b16") if n != cfg.name]
