@@ -322,6 +322,27 @@ __device__ __forceinline__ void stage_scan(const uint8_t* buf, uint32_t fa, int 
     pair_second<TT>(acc1, pk, ct >> 1, bkey, bpair);
 }
 
+// Re-split of a residual pair: for the two fp16 lanes q of the words a (hi),
+// b (lo) and c (chosen codeword), rv = (a + b) - c in fp32 (each operation
+// rounded once, as written), then hi' = fp16(rv) and lo' = fp16(rv - hi'),
+// with the mixed-precision FMAs (fp16 operands read from either half of a
+// word, fp32 arithmetic, an fp16 result written into one half).
+__device__ __forceinline__ void resplit2(uint32_t a, uint32_t b, uint32_t c, uint32_t& na, uint32_t& nb)
+{
+    float t0, t1, r0, r1;
+    asm("v_fma_mix_f32 %0, %1, 1.0, %2 op_sel:[0,0,0] op_sel_hi:[1,0,1]" : "=v"(t0) : "v"(a), "v"(b));
+    asm("v_fma_mix_f32 %0, %1, 1.0, %2 op_sel:[1,0,1] op_sel_hi:[1,0,1]" : "=v"(t1) : "v"(a), "v"(b));
+    asm("v_fma_mix_f32 %0, %1, -1.0, %2 op_sel:[0,0,0] op_sel_hi:[1,0,0]" : "=v"(r0) : "v"(c), "v"(t0));
+    asm("v_fma_mix_f32 %0, %1, -1.0, %2 op_sel:[1,0,0] op_sel_hi:[1,0,0]" : "=v"(r1) : "v"(c), "v"(t1));
+    uint32_t h, l;
+    asm("v_fma_mixlo_f16 %0, %1, 1.0, 0 op_sel_hi:[0,0,0]" : "=&v"(h) : "v"(r0));
+    asm("v_fma_mixhi_f16 %0, %1, 1.0, 0 op_sel_hi:[0,0,0]" : "+v"(h) : "v"(r1));
+    asm("v_fma_mixlo_f16 %0, %1, -1.0, %2 op_sel:[0,0,0] op_sel_hi:[1,0,0]" : "=&v"(l) : "v"(h), "v"(r0));
+    asm("v_fma_mixhi_f16 %0, %1, -1.0, %2 op_sel:[1,0,0] op_sel_hi:[1,0,0]" : "+v"(l) : "v"(h), "v"(r1));
+    na = h;
+    nb = l;
+}
+
 template <int D, bool HILO, bool ENC>
 __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assign_kernel(
     const _Float16* __restrict__ x, const _Float16* __restrict__ books,
@@ -458,13 +479,19 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
                 // r = (hi + lo) - c for st >= 2, (x - c_0) - c_1 for st == 1; split again
 #pragma unroll
                 for (int ks = 0; ks < KS; ++ks) {
+                    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+                    const u32x4 a = __builtin_bit_cast(u32x4, bA[tt][ks]), b = __builtin_bit_cast(u32x4, bB[tt][ks]),
+                                c = __builtin_bit_cast(u32x4, cv[ks]);
+                    u32x4 na, nb;
 #pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        const float rv = (float)bA[tt][ks][e] + (float)bB[tt][ks][e] - (float)cv[ks][e];
-                        const _Float16 h = (_Float16)rv;
-                        bA[tt][ks][e] = h;
-                        bB[tt][ks][e] = (_Float16)(rv - (float)h);
+                    for (int w = 0; w < 4; ++w) {
+                        uint32_t x, y;
+                        resplit2(a[w], b[w], c[w], x, y);
+                        na[w] = x;
+                        nb[w] = y;
                     }
+                    bA[tt][ks] = __builtin_bit_cast(half8, na);
+                    bB[tt][ks] = __builtin_bit_cast(half8, nb);
                 }
             }
             if (last && residual && valid[tt]) {
