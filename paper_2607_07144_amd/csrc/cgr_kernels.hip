@@ -166,12 +166,18 @@ __device__ inline bool decode_finish(double qx, double qy, const double2 P, cons
 }
 
 // Two independent backward walks of `len` steps (LC > 0: the length fixed at
-// compile time, so the loop unrolls fully), symbols into my0 / my1.
+// compile time, so the loop unrolls fully), symbols into my0 / my1.  With an
+// even LC each chain's symbols 2p + 1 and 2p are staged together as one
+// 16-bit write when the staging addresses are even (they are whenever the
+// stream length is), else byte by byte.
 template <int LC, bool EXACT>
 __device__ __forceinline__ void walk_two(double& ax, double& ay, double& bx, double& by, uint8_t* my0, uint8_t* my1,
                                          int len, const Tables& t, const CodecArgs& cd)
 {
+    constexpr bool PACK = LC > 0 && LC % 2 == 0;
     const int n = LC > 0 ? LC : len;
+    const bool even = ((uintptr_t)my0 & 1) == 0;   // my1 - my0 is even
+    uint32_t ha = 0, hb = 0;
 #pragma unroll
     for (int k = n - 1; k >= 0; --k) {
         int ca, cb;
@@ -181,8 +187,21 @@ __device__ __forceinline__ void walk_two(double& ax, double& ay, double& bx, dou
         } else {
             sector_fast2(ax, ay, bx, by, t.lut, cd.lut_bias, ca, cb);
         }
-        my0[k] = (uint8_t)ca;
-        my1[k] = (uint8_t)cb;
+        if (PACK && (k & 1)) {
+            ha = (uint32_t)ca;
+            hb = (uint32_t)cb;
+        } else if (PACK && even) {
+            *(uint16_t*)(my0 + k) = (uint16_t)((ha << 8) | (uint32_t)ca);
+            *(uint16_t*)(my1 + k) = (uint16_t)((hb << 8) | (uint32_t)cb);
+        } else if (PACK) {
+            my0[k] = (uint8_t)ca;
+            my0[k + 1] = (uint8_t)ha;
+            my1[k] = (uint8_t)cb;
+            my1[k + 1] = (uint8_t)hb;
+        } else {
+            my0[k] = (uint8_t)ca;
+            my1[k] = (uint8_t)cb;
+        }
         const double2 wa = t.Wr[ca], wb = t.Wr[cb];
         decode_step(ax, ay, wa, cd.inv_r);
         decode_step(bx, by, wb, cd.inv_r);
