@@ -44,6 +44,7 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <algorithm>
 #include <mutex>
 
 #include "fkv.h"
@@ -570,6 +571,206 @@ constexpr size_t enc_lds_bytes()
     return 256 * 16 + (size_t)Cfg<D>::TOK * 8;
 }
 
+// ---- small books: at most 64 codewords and two stages (d <= 64) ----------
+// Every stage's book then fits in LDS for the whole block, so one block walks
+// several token items of one stream: the books are copied and their norms
+// formed once, no barrier separates the stages, the next item's token rows
+// load while the current item is assigned, and the fused encode of an item
+// needs one barrier (its symbols come from every wave; the symbol staging is
+// double-buffered, so the next item does not wait for the encode).
+constexpr int kSmallK = 64;
+constexpr int kSmallBlocks = 3;   // resident blocks per compute unit
+
+// One stage over the two codeword tiles of a small book with a single
+// fragment buffer.
+template <int D, bool TWO>
+__device__ __forceinline__ void stage_scan_small(const uint8_t* buf, uint32_t fa, const half8 (&bz)[1],
+                                                 const half8 (&bA)[1][Cfg<D>::KS], const half8 (&bB)[1][Cfg<D>::KS],
+                                                 uint32_t (&bkey)[1], int (&bpair)[1])
+{
+    Frag<D> f;
+    floatx16 acc0[1], acc1[1];
+    uint32_t pk[1];
+    load_frag<D>(f, buf, fa, 0);
+    issue_tile<D, 1, TWO>(f, bz, bA, bB, acc0);
+    load_frag<D>(f, buf, fa, 1);
+    issue_tile<D, 1, TWO>(f, bz, bA, bB, acc1);
+    pair_first<1>(acc0, pk);
+    pair_second<1>(acc1, pk, 0, bkey, bpair);
+}
+
+template <int D>
+__device__ __forceinline__ void load_rows(half8 (&dst)[Cfg<D>::KS], const _Float16* __restrict__ x, int64_t row,
+                                          bool valid, int hh)
+{
+    const _Float16* p = x + row * D + 8 * hh;
+#pragma unroll
+    for (int ks = 0; ks < Cfg<D>::KS; ++ks) dst[ks] = valid ? *(const half8*)(p + 16 * ks) : (half8)(_Float16)0;
+}
+
+template <int D, bool ENC>
+__global__ __launch_bounds__(Cfg<D>::THREADS, kSmallBlocks) void rvq_small_kernel(
+    const _Float16* __restrict__ x, const _Float16* __restrict__ books, const int32_t* __restrict__ stream_book,
+    uint8_t* __restrict__ symbols, float* __restrict__ residual, uint32_t* __restrict__ n_bad, int64_t T,
+    int64_t t_begin, int64_t Ta, int S, int K, int Kp, int n_books, int64_t blocks_per_stream, int64_t tpi,
+    int64_t ipb, double2* __restrict__ points, const double2* __restrict__ vtab, double cr, int cN, int cL,
+    int64_t n_spans)
+{
+    using C = Cfg<D>;
+    constexpr int KS = C::KS, TOK = C::WAVES * 32;
+    extern __shared__ __align__(16) uint8_t lds[];
+    const size_t buf_bytes = buf_bytes_of(C::ROW_P, Kp);
+
+    // XCD-aware order, as in rvq_assign_kernel
+    const uint32_t nblk = gridDim.x, q8 = nblk / 8, r8 = nblk % 8;
+    const uint32_t xcd = blockIdx.x % 8, slot = blockIdx.x / 8;
+    const int64_t item = (int64_t)xcd * q8 + min(xcd, r8) + slot;
+    const int64_t s = item / blocks_per_stream;
+    const int64_t tb0 = (item - s * blocks_per_stream) * ipb * tpi;   // the block's first token
+    const int64_t te0 = min(Ta, tb0 + ipb * tpi);                      // one past its last
+
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int col = lane & 31, hh = lane >> 5;
+    uint8_t* sym_s = symbols + s * Ta * S;
+    const int b = stream_book[s];
+    const _Float16* xs = x + (s * T + t_begin) * D;
+
+    half8 bA[1][KS], nA[KS];   // token rows of the current and the next item
+    load_rows<D>(bA[0], xs, tb0 + wave * 32 + col, tb0 + wave * 32 + col < min(te0, tb0 + tpi), hh);
+
+    if (b < 0 || b >= n_books) {
+        for (int64_t i = tb0 * S + tid; i < te0 * S; i += C::THREADS) sym_s[i] = 0xFF;
+        if (ENC)
+            for (int64_t j = tb0 * S / cL + tid; j < (te0 * S + cL - 1) / cL; j += C::THREADS)
+                points[s * n_spans + j] = make_double2(NAN, NAN);
+        if (residual)
+            for (int64_t i = tb0 * D + tid; i < te0 * D; i += C::THREADS) residual[s * Ta * D + i] = NAN;
+        if (tid == 0 && tb0 == 0 && n_bad) atomicAdd(n_bad, 1u);
+        return;
+    }
+    const _Float16* bk = books + (int64_t)b * S * K * D;
+
+    double2* V_l = (double2*)(lds + 2 * buf_bytes);
+    uint8_t* sym_l = (uint8_t*)(V_l + 256);   // two item buffers of TOK * S bytes
+    if (ENC && tid < 256) V_l[tid] = tid < cN ? vtab[tid] : make_double2(NAN, NAN);
+    book_to_lds_async<D>(bk, K, Kp, lds, wave, lane);
+    if (S > 1) book_to_lds_async<D>(bk + (size_t)K * D, K, Kp, lds + buf_bytes, wave, lane);
+    if (tid < 2) *(half8*)(lds + tid * buf_bytes + (size_t)Kp * C::ROW_P) = (half8)(_Float16)0;
+    wait_all_and_sync();
+    if (S > 1)
+        book_bias_rows<D, 2>(lds, lds + buf_bytes, Kp);
+    else
+        book_bias_rows<D, 1>(lds, lds, Kp);
+    __syncthreads();
+
+    const uint32_t fa = (uint32_t)(col * C::ROW_P + hh * 16);
+    int it = 0;
+    for (int64_t tb = tb0; tb < te0; tb += tpi, ++it) {
+        const int64_t te = min(te0, tb + tpi);
+        const int64_t tok = tb + wave * 32 + col;
+        const bool valid = tok < te;
+        const int64_t tbn = tb + tpi;
+        const bool more = tbn < te0;
+        if (more) load_rows<D>(nA, xs, tbn + wave * 32 + col, tbn + wave * 32 + col < min(te0, tbn + tpi), hh);
+
+        half8 bz[1], bB[1][KS];
+        float n2 = 0.0f;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            bB[0][ks] = (half8)(_Float16)0;
+#pragma unroll
+            for (int e = 0; e < 8; e += 2) {
+                const half2 h = {bA[0][ks][e], bA[0][ks][e + 1]};
+                n2 = __builtin_amdgcn_fdot2(h, h, n2, false);
+            }
+        }
+        n2 += __uint_as_float(lane_xor32(__float_as_uint(n2), hh));
+        bz[0] = bias_column(0.5f * n2 * (1.0f + 0x1p-10f), hh);
+        uint8_t* syl = sym_l + (it & 1) * TOK * S;
+
+        for (int st = 0; st < S; ++st) {
+            const uint8_t* buf = lds + st * buf_bytes;
+            uint32_t bkey[1] = {0xFFFFFFFFu};
+            int bpair[1] = {0};
+            if (st > 0)
+                stage_scan_small<D, true>(buf, fa, bz, bA, bB, bkey, bpair);
+            else
+                stage_scan_small<D, false>(buf, fa, bz, bA, bB, bkey, bpair);
+            const int li = (int)(bkey[0] & 31u);
+            int cw = (li >> 4) * 32 + 8 * ((li & 15) >> 2) + 4 * hh + (li & 3);
+            cw = min(cw, K - 1);  // only reachable with all-NaN scores; keeps reads in bounds
+            uint32_t val = bkey[0] & ~31u;
+            const uint32_t oval = lane_xor32(val, hh);
+            const int ocw = (int)lane_xor32((uint32_t)cw, hh);
+            if (oval < val || (oval == val && ocw < cw)) {
+                val = oval;
+                cw = ocw;
+            }
+            if (hh == 0 && valid) {
+                sym_s[tok * S + st] = (uint8_t)cw;
+                if (ENC) syl[(tok - tb) * S + st] = (uint8_t)cw;
+            }
+            bz[0] = bias_column(-__uint_as_float(val) * (1.0f + 0x1p-10f), hh);
+            half8 cv[KS];
+            const uint8_t* crow = buf + (size_t)cw * C::ROW_P + hh * 16;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) cv[ks] = *(const half8*)(crow + ks * 32);
+            const bool last = st + 1 == S;
+            if (last && residual && valid) {
+                float* out = residual + (s * Ta + tok) * D + 8 * hh;
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) {
+                    floatx4 lo4, hi4;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const float rv = (float)bA[0][ks][e] + (st > 0 ? (float)bB[0][ks][e] : 0.0f) -
+                                         (float)cv[ks][e];
+                        if (e < 4) lo4[e] = rv; else hi4[e - 4] = rv;
+                    }
+                    *(floatx4*)(out + 16 * ks) = lo4;
+                    *(floatx4*)(out + 16 * ks + 4) = hi4;
+                }
+            }
+            if (st == 0 && !last) {
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) bB[0][ks] = -cv[ks];
+            }
+        }
+        if (ENC) {
+            // the item's token range holds whole spans (tpi is a multiple of
+            // L / gcd(L, S)), each walked from the anchor (0,0) with
+            // p <- V + r (p - V), operation for operation as the encode kernel
+            __syncthreads();
+            const int64_t n_sym = Ta * S;
+            for (int64_t j = tb * S / cL + tid; j < (te * S + cL - 1) / cL; j += C::THREADS) {
+                const int64_t a = j * cL;
+                const int len = (int)min((int64_t)cL, n_sym - a);
+                const uint8_t* my = syl + (a - tb * S);
+                double px = 0.0, py = 0.0;
+                for (int k0 = 0; k0 < len; k0 += 8) {
+                    double2 v[8];
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) v[u] = k0 + u < len ? V_l[my[k0 + u]] : make_double2(0.0, 0.0);
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) {
+                        if (k0 + u < len) {
+                            const double tx = px - v[u].x, ty = py - v[u].y;
+                            const double ux = cr * tx, uy = cr * ty;
+                            px = v[u].x + ux;
+                            py = v[u].y + uy;
+                        }
+                    }
+                }
+                points[s * n_spans + j] = make_double2(px, py);
+            }
+        }
+        if (more) {
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) bA[0][ks] = nA[ks];
+        }
+    }
+}
+
 // Fused encode parameters (points == nullptr: assignment only).
 struct EncArgs {
     double2* points;
@@ -617,11 +818,57 @@ int launch_rvq_t(const fkv_rvq_desc* dsc, const uint16_t* x, const uint16_t* boo
     return launch_status();
 }
 
+// Small books: token items of 128 (whole spans with the fused encode) per
+// wave set, several per block, blocks balanced within a stream so that the
+// grid is about four rounds of resident blocks.
+template <int D, bool ENC>
+int launch_rvq_small(const fkv_rvq_desc* dsc, const uint16_t* x, const uint16_t* books,
+                     const int32_t* stream_book, uint8_t* symbols, float* residual, uint32_t* n_bad,
+                     const EncArgs& enc, hipStream_t stream)
+{
+    constexpr int TOK = Cfg<D>::WAVES * 32;
+    const int Kp = 64;
+    const int64_t Ta = dsc->t_end - dsc->t_begin;
+    int64_t tpi = TOK;
+    if (ENC) {
+        int a = enc.L, b = dsc->S;
+        while (b) {
+            const int t = a % b;
+            a = b;
+            b = t;
+        }
+        const int unit = enc.L / a;
+        if (unit > TOK) return FKV_ERR_UNSUPPORTED;
+        tpi = (int64_t)(TOK / unit) * unit;
+    }
+    const int64_t ips = (Ta + tpi - 1) / tpi;                   // items per stream
+    const int64_t target = 256 * kSmallBlocks * 4;             // about four rounds of resident blocks
+    const int64_t want = (dsc->n_streams * ips + target - 1) / target;
+    const int64_t bps = (ips + std::max<int64_t>(1, want) - 1) / std::max<int64_t>(1, want);   // blocks per stream
+    const int64_t ipb = (ips + bps - 1) / bps;                 // items per block
+    const int64_t nblk = bps * dsc->n_streams;
+    if (nblk > 0x7fffffff) return FKV_ERR_UNSUPPORTED;
+    const int64_t n_spans = ENC ? (Ta * dsc->S + enc.L - 1) / enc.L : 0;
+    const size_t shm = 2 * buf_bytes_of(Cfg<D>::ROW_P, Kp) + (ENC ? 256 * 16 + 2 * TOK * 8 : 0);
+    hipLaunchKernelGGL((rvq_small_kernel<D, ENC>), dim3((unsigned)nblk), dim3(Cfg<D>::THREADS), shm, stream,
+                       (const _Float16*)x, (const _Float16*)books, stream_book, symbols, residual, n_bad, dsc->T,
+                       dsc->t_begin, Ta, dsc->S, dsc->K, Kp, dsc->n_books, bps, tpi, ipb, enc.points, enc.vtab, enc.r,
+                       enc.N, enc.L, n_spans);
+    return launch_status();
+}
+
 template <int D>
 int launch_rvq(const fkv_rvq_desc* dsc, const uint16_t* x, const uint16_t* books,
                const int32_t* stream_book, uint8_t* symbols, float* residual, uint32_t* n_bad,
                const EncArgs& enc, hipStream_t stream)
 {
+    if constexpr (D <= 64) {
+        if (dsc->K <= kSmallK && dsc->S <= 2) {
+            if (enc.points)
+                return launch_rvq_small<D, true>(dsc, x, books, stream_book, symbols, residual, n_bad, enc, stream);
+            return launch_rvq_small<D, false>(dsc, x, books, stream_book, symbols, residual, n_bad, enc, stream);
+        }
+    }
     if (enc.points) {
         if (dsc->S <= 2)
             return launch_rvq_t<D, false, true>(dsc, x, books, stream_book, symbols, residual, n_bad, enc, stream);

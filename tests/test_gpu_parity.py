@@ -207,6 +207,8 @@ def test_rvq_gpt2_config_full(fkv, orc):
     (160, 5, 96, 60, 3, 60), (176, 2, 255, 40, 0, 40), (192, 3, 256, 50, 0, 50),
     (208, 2, 130, 33, 0, 33), (224, 4, 64, 45, 5, 45), (240, 2, 100, 40, 0, 40),
     (256, 3, 256, 70, 2, 70), (128, 8, 256, 80, 0, 80), (32, 6, 17, 300, 10, 290),
+    # small books (K <= 64, S <= 2, d <= 64): several token items per block, a ragged last item
+    (64, 1, 40, 300, 3, 297), (32, 2, 7, 1500, 0, 1500), (64, 2, 64, 700, 4, 668),
 ])
 def test_rvq_shapes(fkv, orc, d, S, K, T, t0, t1):
     rng = np.random.default_rng(d * 7 + S * 13 + K)
