@@ -574,12 +574,12 @@ constexpr size_t enc_lds_bytes()
 // ---- small books: at most 64 codewords and two stages (d <= 64) ----------
 // Every stage's book then fits in LDS for the whole block, so one block walks
 // several token items of one stream: the books are copied and their norms
-// formed once, no barrier separates the stages, the next item's token rows
-// load while the current item is assigned, and the fused encode of an item
-// needs one barrier (its symbols come from every wave; the symbol staging is
-// double-buffered, so the next item does not wait for the encode).
+// formed once, no barrier separates the stages or the items, and the next
+// item's token rows load while the current item is assigned.  The block's
+// symbols are staged in LDS and its spans encoded once, after its last item.
 constexpr int kSmallK = 64;
-constexpr int kSmallBlocks = 3;   // resident blocks per compute unit
+constexpr int kSmallBlocks = 3;     // resident blocks per compute unit
+constexpr int kSmallMaxItems = 8;   // token items per block (bounds the symbol staging)
 
 // One stage over the two codeword tiles of a small book with a single
 // fragment buffer.
@@ -597,6 +597,14 @@ __device__ __forceinline__ void stage_scan_small(const uint8_t* buf, uint32_t fa
     issue_tile<D, 1, TWO>(f, bz, bA, bB, acc1);
     pair_first<1>(acc0, pk);
     pair_second<1>(acc1, pk, 0, bkey, bpair);
+}
+
+// A block barrier that orders LDS only: each wave's LDS operations complete
+// before it, while its global loads (the next item's token rows) and stores
+// stay in flight (__syncthreads also waits for those).
+__device__ __forceinline__ void lds_barrier()
+{
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
 template <int D>
@@ -635,7 +643,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, kSmallBlocks) void rvq_small_kerne
     const int b = stream_book[s];
     const _Float16* xs = x + (s * T + t_begin) * D;
 
-    half8 bA[1][KS], nA[KS];   // token rows of the current and the next item
+    half8 bA[1][KS];   // token rows of the block's first item
     load_rows<D>(bA[0], xs, tb0 + wave * 32 + col, tb0 + wave * 32 + col < min(te0, tb0 + tpi), hh);
 
     if (b < 0 || b >= n_books) {
@@ -651,7 +659,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, kSmallBlocks) void rvq_small_kerne
     const _Float16* bk = books + (int64_t)b * S * K * D;
 
     double2* V_l = (double2*)(lds + 2 * buf_bytes);
-    uint8_t* sym_l = (uint8_t*)(V_l + 256);   // two item buffers of TOK * S bytes
+    uint8_t* sym_l = (uint8_t*)(V_l + 256);   // the block's symbols, token-major from tb0
     if (ENC && tid < 256) V_l[tid] = tid < cN ? vtab[tid] : make_double2(NAN, NAN);
     book_to_lds_async<D>(bk, K, Kp, lds, wave, lane);
     if (S > 1) book_to_lds_async<D>(bk + (size_t)K * D, K, Kp, lds + buf_bytes, wave, lane);
@@ -664,14 +672,15 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, kSmallBlocks) void rvq_small_kerne
     __syncthreads();
 
     const uint32_t fa = (uint32_t)(col * C::ROW_P + hh * 16);
-    int it = 0;
-    for (int64_t tb = tb0; tb < te0; tb += tpi, ++it) {
+    // One token item on rows `cur`; the next item's rows load into `nxt`
+    // (the two register sets alternate, so the load is first waited for when
+    // the next item starts).
+    auto run_item = [&](int64_t tb, half8 (&cur)[1][KS], half8 (&nxt)[1][KS]) {
         const int64_t te = min(te0, tb + tpi);
         const int64_t tok = tb + wave * 32 + col;
         const bool valid = tok < te;
         const int64_t tbn = tb + tpi;
-        const bool more = tbn < te0;
-        if (more) load_rows<D>(nA, xs, tbn + wave * 32 + col, tbn + wave * 32 + col < min(te0, tbn + tpi), hh);
+        if (tbn < te0) load_rows<D>(nxt[0], xs, tbn + wave * 32 + col, tbn + wave * 32 + col < min(te0, tbn + tpi), hh);
 
         half8 bz[1], bB[1][KS];
         float n2 = 0.0f;
@@ -680,22 +689,21 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, kSmallBlocks) void rvq_small_kerne
             bB[0][ks] = (half8)(_Float16)0;
 #pragma unroll
             for (int e = 0; e < 8; e += 2) {
-                const half2 h = {bA[0][ks][e], bA[0][ks][e + 1]};
+                const half2 h = {cur[0][ks][e], cur[0][ks][e + 1]};
                 n2 = __builtin_amdgcn_fdot2(h, h, n2, false);
             }
         }
         n2 += __uint_as_float(lane_xor32(__float_as_uint(n2), hh));
         bz[0] = bias_column(0.5f * n2 * (1.0f + 0x1p-10f), hh);
-        uint8_t* syl = sym_l + (it & 1) * TOK * S;
 
         for (int st = 0; st < S; ++st) {
             const uint8_t* buf = lds + st * buf_bytes;
             uint32_t bkey[1] = {0xFFFFFFFFu};
             int bpair[1] = {0};
             if (st > 0)
-                stage_scan_small<D, true>(buf, fa, bz, bA, bB, bkey, bpair);
+                stage_scan_small<D, true>(buf, fa, bz, cur, bB, bkey, bpair);
             else
-                stage_scan_small<D, false>(buf, fa, bz, bA, bB, bkey, bpair);
+                stage_scan_small<D, false>(buf, fa, bz, cur, bB, bkey, bpair);
             const int li = (int)(bkey[0] & 31u);
             int cw = (li >> 4) * 32 + 8 * ((li & 15) >> 2) + 4 * hh + (li & 3);
             cw = min(cw, K - 1);  // only reachable with all-NaN scores; keeps reads in bounds
@@ -708,7 +716,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, kSmallBlocks) void rvq_small_kerne
             }
             if (hh == 0 && valid) {
                 sym_s[tok * S + st] = (uint8_t)cw;
-                if (ENC) syl[(tok - tb) * S + st] = (uint8_t)cw;
+                if (ENC) sym_l[(tok - tb0) * S + st] = (uint8_t)cw;
             }
             bz[0] = bias_column(-__uint_as_float(val) * (1.0f + 0x1p-10f), hh);
             half8 cv[KS];
@@ -723,7 +731,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, kSmallBlocks) void rvq_small_kerne
                     floatx4 lo4, hi4;
 #pragma unroll
                     for (int e = 0; e < 8; ++e) {
-                        const float rv = (float)bA[0][ks][e] + (st > 0 ? (float)bB[0][ks][e] : 0.0f) -
+                        const float rv = (float)cur[0][ks][e] + (st > 0 ? (float)bB[0][ks][e] : 0.0f) -
                                          (float)cv[ks][e];
                         if (e < 4) lo4[e] = rv; else hi4[e - 4] = rv;
                     }
@@ -736,37 +744,38 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, kSmallBlocks) void rvq_small_kerne
                 for (int ks = 0; ks < KS; ++ks) bB[0][ks] = -cv[ks];
             }
         }
-        if (ENC) {
-            // the item's token range holds whole spans (tpi is a multiple of
-            // L / gcd(L, S)), each walked from the anchor (0,0) with
-            // p <- V + r (p - V), operation for operation as the encode kernel
-            __syncthreads();
-            const int64_t n_sym = Ta * S;
-            for (int64_t j = tb * S / cL + tid; j < (te * S + cL - 1) / cL; j += C::THREADS) {
-                const int64_t a = j * cL;
-                const int len = (int)min((int64_t)cL, n_sym - a);
-                const uint8_t* my = syl + (a - tb * S);
-                double px = 0.0, py = 0.0;
-                for (int k0 = 0; k0 < len; k0 += 8) {
-                    double2 v[8];
+    };
+    half8 rB[1][KS];
+    for (int64_t tb = tb0; tb < te0; tb += 2 * tpi) {
+        run_item(tb, bA, rB);
+        if (tb + tpi < te0) run_item(tb + tpi, rB, bA);
+    }
+    if (ENC) {
+        // the block's token range holds whole spans (tpi is a multiple of
+        // L / gcd(L, S)), each walked from the anchor (0,0) with
+        // p <- V + r (p - V), operation for operation as the encode kernel
+        lds_barrier();
+        const int64_t n_sym = Ta * S;
+        for (int64_t j = tb0 * S / cL + tid; j < (te0 * S + cL - 1) / cL; j += C::THREADS) {
+            const int64_t a = j * cL;
+            const int len = (int)min((int64_t)cL, n_sym - a);
+            const uint8_t* my = sym_l + (a - tb0 * S);
+            double px = 0.0, py = 0.0;
+            for (int k0 = 0; k0 < len; k0 += 8) {
+                double2 v[8];
 #pragma unroll
-                    for (int u = 0; u < 8; ++u) v[u] = k0 + u < len ? V_l[my[k0 + u]] : make_double2(0.0, 0.0);
+                for (int u = 0; u < 8; ++u) v[u] = k0 + u < len ? V_l[my[k0 + u]] : make_double2(0.0, 0.0);
 #pragma unroll
-                    for (int u = 0; u < 8; ++u) {
-                        if (k0 + u < len) {
-                            const double tx = px - v[u].x, ty = py - v[u].y;
-                            const double ux = cr * tx, uy = cr * ty;
-                            px = v[u].x + ux;
-                            py = v[u].y + uy;
-                        }
+                for (int u = 0; u < 8; ++u) {
+                    if (k0 + u < len) {
+                        const double tx = px - v[u].x, ty = py - v[u].y;
+                        const double ux = cr * tx, uy = cr * ty;
+                        px = v[u].x + ux;
+                        py = v[u].y + uy;
                     }
                 }
-                points[s * n_spans + j] = make_double2(px, py);
             }
-        }
-        if (more) {
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) bA[0][ks] = nA[ks];
+            points[s * n_spans + j] = make_double2(px, py);
         }
     }
 }
@@ -843,13 +852,13 @@ int launch_rvq_small(const fkv_rvq_desc* dsc, const uint16_t* x, const uint16_t*
     }
     const int64_t ips = (Ta + tpi - 1) / tpi;                   // items per stream
     const int64_t target = 256 * kSmallBlocks * 4;             // about four rounds of resident blocks
-    const int64_t want = (dsc->n_streams * ips + target - 1) / target;
-    const int64_t bps = (ips + std::max<int64_t>(1, want) - 1) / std::max<int64_t>(1, want);   // blocks per stream
+    const int64_t want = std::min<int64_t>(kSmallMaxItems, std::max<int64_t>(1, (dsc->n_streams * ips + target - 1) / target));
+    const int64_t bps = (ips + want - 1) / want;               // blocks per stream
     const int64_t ipb = (ips + bps - 1) / bps;                 // items per block
     const int64_t nblk = bps * dsc->n_streams;
     if (nblk > 0x7fffffff) return FKV_ERR_UNSUPPORTED;
     const int64_t n_spans = ENC ? (Ta * dsc->S + enc.L - 1) / enc.L : 0;
-    const size_t shm = 2 * buf_bytes_of(Cfg<D>::ROW_P, Kp) + (ENC ? 256 * 16 + 2 * TOK * 8 : 0);
+    const size_t shm = 2 * buf_bytes_of(Cfg<D>::ROW_P, Kp) + (ENC ? 256 * 16 + (size_t)kSmallMaxItems * TOK * 2 : 0);
     hipLaunchKernelGGL((rvq_small_kernel<D, ENC>), dim3((unsigned)nblk), dim3(Cfg<D>::THREADS), shm, stream,
                        (const _Float16*)x, (const _Float16*)books, stream_book, symbols, residual, n_bad, dsc->T,
                        dsc->t_begin, Ta, dsc->S, dsc->K, Kp, dsc->n_books, bps, tpi, ipb, enc.points, enc.vtab, enc.r,
