@@ -106,18 +106,21 @@ def test_fused_long_context_sample(fkv, orc):
     torch.cuda.empty_cache()
 
 
-def test_fused_invalid_book_and_ragged(fkv):
-    rng = np.random.default_rng(8)
-    ns, T, d, S, K, N = 5, 300, 32, 3, 40, 64       # L = 9: 9-token units, a ragged last block
+@pytest.mark.parametrize("S,T", [(3, 300), (2, 1400)])
+def test_fused_invalid_book_and_ragged(fkv, S, T):
+    """An invalid book id and a ragged last block; S = 2 runs the small-book kernel (several token
+    items per block), S = 3 the general one."""
+    rng = np.random.default_rng(8 + S)
+    ns, d, K, N = 5, 32, 40, 64                     # L = 9: 9-token units, a ragged last block
     x = torch.from_numpy(rng.standard_normal((ns, T, d)).astype(np.float16)).cuda()
     books = torch.from_numpy((rng.standard_normal((2, S, K, d)) * 0.7).astype(np.float16)).cuda()
     sb = torch.tensor([0, 7, 1, 1, 0], dtype=torch.int32, device="cuda")       # stream 1: invalid book
     codec = fkv.Codec(N)
     nb1 = torch.zeros(1, dtype=torch.int32, device="cuda")
     nb2 = torch.zeros(1, dtype=torch.int32, device="cuda")
-    sym, _ = fkv.fkv_rvq_assign(x, books, sb, 2, 283, n_bad=nb1)
+    sym, _ = fkv.fkv_rvq_assign(x, books, sb, 2, T - 17, n_bad=nb1)
     pts = fkv.fkv_cgr_encode_spans(codec, sym)
-    fs, fp, _ = fkv.fkv_rvq_assign_encode(codec, x, books, sb, 2, 283, n_bad=nb2)
+    fs, fp, _ = fkv.fkv_rvq_assign_encode(codec, x, books, sb, 2, T - 17, n_bad=nb2)
     assert torch.equal(fs, sym) and int(nb1.item()) == int(nb2.item()) == 1
     a, b = host(fp), host(pts)
     assert np.isnan(a[1]).all() and np.isnan(b[1]).all()
@@ -126,7 +129,10 @@ def test_fused_invalid_book_and_ragged(fkv):
 
 
 @pytest.mark.parametrize("d,S,K,N,T", [(16, 1, 16, 16, 400), (48, 3, 64, 64, 333), (128, 2, 256, 256, 700),
-                                       (256, 3, 200, 256, 300), (96, 5, 32, 3, 260), (64, 8, 256, 256, 257)])
+                                       (256, 3, 200, 256, 300), (96, 5, 32, 3, 260), (64, 8, 256, 256, 257),
+                                       # small books: many token items per block, 8-token span units,
+                                       # symbols beyond the alphabet
+                                       (64, 2, 64, 64, 1500), (32, 2, 20, 16, 900), (48, 2, 64, 16, 500)])
 def test_fused_shapes(fkv, d, S, K, N, T):
     """Random books and inputs over head dims, stage counts and alphabets (L from 6 to 44)."""
     rng = np.random.default_rng(d + 17 * S + N)
