@@ -23,7 +23,8 @@ def _search(fkv, codec, traj, q, verify, max_hits=1 << 16):
     return sorted(map(tuple, got.tolist())), n, int(nc.item())
 
 
-@pytest.mark.parametrize("N,W", [(16, 0), (64, 0), (256, 0), (3, 64), (256, 11), (256, 1), (64, 16), (64, 17)])
+@pytest.mark.parametrize("N,W", [(16, 0), (64, 0), (256, 0), (3, 64), (256, 11), (256, 1), (64, 16), (64, 17),
+                                 (256, 8), (64, 5), (16, 2)])
 def test_trajectory_matches_oracle(fkv, orc, N, W):
     rng = np.random.default_rng(N + W)
     sym = rng.integers(0, N, (5, 1000 + 37), dtype=np.uint8)     # a ragged last tile
@@ -31,6 +32,18 @@ def test_trajectory_matches_oracle(fkv, orc, N, W):
     Wv = W or codec.L
     tr = fkv.fkv_trajectory(codec, torch.from_numpy(sym).cuda(), Wv)
     want = orc.trajectory(orc.Codec(N), sym, Wv)
+    assert np.array_equal(host(tr).view(np.uint64), want.view(np.uint64))
+
+
+@pytest.mark.parametrize("n_sym,W", [(1, 6), (3, 6), (5, 6), (6, 6), (7, 8), (255, 6), (256, 6), (257, 8),
+                                     (1023, 6), (1024, 3), (1025, 8)])
+def test_trajectory_short_streams(fkv, orc, n_sym, W):
+    """Streams shorter than, equal to and just past the window, and around the 256-position tile."""
+    rng = np.random.default_rng(n_sym * 3 + W)
+    sym = rng.integers(0, 256, (3, n_sym), dtype=np.uint8)
+    codec = fkv.Codec(256)
+    tr = fkv.fkv_trajectory(codec, torch.from_numpy(sym).cuda(), W)
+    want = orc.trajectory(orc.Codec(256), sym, W)
     assert np.array_equal(host(tr).view(np.uint64), want.view(np.uint64))
 
 
