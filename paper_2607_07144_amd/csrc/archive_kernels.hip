@@ -165,7 +165,7 @@ __global__ __launch_bounds__(kBlock) void trajectory_kernel(const uint8_t* __res
             const uint8_t* my = tile + (g0 & 3) + (a - a0);
             double px = 0.0, py = 0.0;
             for (int64_t j = 0; j <= k - a; ++j) encode_step(px, py, V[my[j]], cd.r);
-            traj[s * n_sym + k] = make_double2(px, py);
+            store_point_stream(traj + s * n_sym + k, px, py);
         }
     }
 }
@@ -204,7 +204,7 @@ __global__ __launch_bounds__(kBlock) void suffix_search_kernel(
             s = i / n_sym;
             k = i - s * n_sym;
             if (qok && k >= ell - 1) {
-                const double2 p = traj[i];
+                const double2 p = load_point_stream(traj + i);
                 const double dx = p.x - qx, dy = p.y - qy;
                 const double d2 = dx * dx + dy * dy;
                 cand = d2 <= thr2;

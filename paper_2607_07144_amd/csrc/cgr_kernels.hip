@@ -63,16 +63,17 @@ __global__ __launch_bounds__(kBlock, 8) void cgr_encode_tiles_kernel(
             const uint8_t* my = tile + (g0 & 3) + threadIdx.x * L;
             double px = 0.0, py = 0.0;
             for (int k = 0; k < len; ++k) encode_step(px, py, V[my[k]], cd.r);
-            pts[s * n_spans + j0 + threadIdx.x] = make_double2(px, py);
+            store_point_stream(pts + s * n_spans + j0 + threadIdx.x, px, py);
         }
     }
 }
 
 // Span encode for spans of up to 16 symbols, with no LDS staging: a wave
-// takes 128 consecutive spans of one stream (a wave tile), two per lane (j and
-// j + 64), loads the aligned dwords that cover each span, extracts the symbols
-// and walks both spans from the anchor as two independent chains.  Wave tiles
-// are walked without division.
+// takes 256 consecutive spans of one stream (a wave tile), four per lane (j,
+// j + 64, j + 128, j + 192), loads the aligned dwords that cover each span,
+// extracts the symbols and walks the four spans from the anchor as independent
+// chains; the points go out with streaming stores.  Wave tiles are walked
+// without division.
 constexpr int kEncSpl = 4;
 constexpr int kEncTile = 64 * kEncSpl;
 
@@ -136,7 +137,7 @@ __global__ __launch_bounds__(kBlock, 8) void cgr_encode_kernel(
                 if (k < len[h]) encode_step(px[h], py[h], V[(e[h][k >> 2] >> (8 * (k & 3))) & 0xFF], cd.r);
 #pragma unroll
         for (int h = 0; h < kEncSpl; ++h)
-            if (len[h] > 0) pts[w.s * n_spans + jj[h]] = make_double2(px[h], py[h]);
+            if (len[h] > 0) store_point_stream(pts + w.s * n_spans + jj[h], px[h], py[h]);
     }
 }
 
@@ -147,7 +148,8 @@ __global__ __launch_bounds__(kBlock, 8) void cgr_encode_kernel(
 // independent chains so that the look-ups of one overlap the arithmetic of
 // the other, into its own LDS staging area, and writes them back as aligned
 // dwords (bytes at either end); the points of its next wave tile are loaded
-// while the current one decodes.
+// while the current one decodes.  Points are read and symbols written with
+// streaming accesses: each is touched once, and the tables stay in LDS.
 constexpr int kDecodeSpl = 2;                  // spans per lane
 constexpr int kDecodeTile = 64 * kDecodeSpl;   // spans per wave tile
 
@@ -230,8 +232,8 @@ __global__ __launch_bounds__(kBlock, 8) void cgr_decode_kernel(
     double2 P0 = zero, P1 = zero;
     if (wave < n_wtiles) {
         const int64_t j = cur.j * kDecodeTile + lane;
-        if (j < n_spans) P0 = pts[cur.s * n_spans + j];
-        if (j + 64 < n_spans) P1 = pts[cur.s * n_spans + j + 64];
+        if (j < n_spans) P0 = load_point_stream(pts + cur.s * n_spans + j);
+        if (j + 64 < n_spans) P1 = load_point_stream(pts + cur.s * n_spans + j + 64);
     }
     Tables t = stage_tables(gtab, N, lds, VERIFY, EXACT);
     uint8_t* stage = lds + staged_table_bytes(N, VERIFY, EXACT) + (size_t)wv * stage_bytes;
@@ -245,8 +247,8 @@ __global__ __launch_bounds__(kBlock, 8) void cgr_decode_kernel(
         double2 N0 = zero, N1 = zero;
         if (tw + n_waves < n_wtiles) {
             const int64_t j = nxt.j * kDecodeTile + lane;
-            if (j < n_spans) N0 = pts[nxt.s * n_spans + j];
-            if (j + 64 < n_spans) N1 = pts[nxt.s * n_spans + j + 64];
+            if (j < n_spans) N0 = load_point_stream(pts + nxt.s * n_spans + j);
+            if (j + 64 < n_spans) N1 = load_point_stream(pts + nxt.s * n_spans + j + 64);
         }
         uint8_t* my0 = stage + (g0 & 3) + lane * L;
         uint8_t* my1 = my0 + 64 * L;
@@ -288,7 +290,7 @@ __global__ __launch_bounds__(kBlock, 8) void cgr_decode_kernel(
         // the wave's LDS writes above precede its reads below (a wave's LDS
         // operations are performed in order)
         __builtin_amdgcn_wave_barrier();
-        lds_to_bytes_wave(stage, g0, g1, sym, lane);
+        lds_to_bytes_wave<true>(stage, g0, g1, sym, lane);
         P0 = N0;
         P1 = N1;
     }

@@ -19,6 +19,22 @@ inline int launch_status()
 
 inline bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
 
+// Streaming (non-temporal) 16-byte point load and store: the access carries
+// the non-temporal hint, so lines that a kernel touches exactly once do not
+// displace what it re-reads (its tables, the symbol lines that neighbouring
+// lanes share).  Values are those of a plain access.
+typedef double fkv_v2d __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ double2 load_point_stream(const double2* p)
+{
+    const fkv_v2d v = __builtin_nontemporal_load((const fkv_v2d*)p);
+    return make_double2(v.x, v.y);
+}
+__device__ __forceinline__ void store_point_stream(double2* p, double x, double y)
+{
+    const fkv_v2d v = {x, y};
+    __builtin_nontemporal_store(v, (fkv_v2d*)p);
+}
+
 // Copies global bytes [g0, g1) of `src` into LDS so that global byte g sits at
 // LDS byte (g - (g0 & ~3)).  Whole aligned dwords are moved as dwords; the
 // partial dwords at either end byte by byte, so nothing outside [g0, g1) is
@@ -61,8 +77,10 @@ __device__ inline void lds_to_bytes(const uint8_t* lds, int64_t g0, int64_t g1,
 }
 
 // One wave's counterpart of lds_to_bytes: its 64 lanes write LDS bytes back to
-// global [g0, g1), whole aligned dwords as dwords and the partial dwords at
-// either end byte by byte (so nothing outside [g0, g1) is written).
+// global [g0, g1), whole aligned dwords as dwords (streaming stores when NT)
+// and the partial dwords at either end byte by byte (so nothing outside
+// [g0, g1) is written).
+template <bool NT = false>
 __device__ inline void lds_to_bytes_wave(const uint8_t* lds, int64_t g0, int64_t g1, uint8_t* __restrict__ dst,
                                          int lane)
 {
@@ -75,7 +93,12 @@ __device__ inline void lds_to_bytes_wave(const uint8_t* lds, int64_t g0, int64_t
     }
     uint32_t* d32 = (uint32_t*)dst;
     const uint32_t* l32 = (const uint32_t*)(lds + (a0 - base));
-    for (int64_t w = (a0 >> 2) + lane; w < (a1 >> 2); w += 64) d32[w] = l32[w - (a0 >> 2)];
+    for (int64_t w = (a0 >> 2) + lane; w < (a1 >> 2); w += 64) {
+        if (NT)
+            __builtin_nontemporal_store(l32[w - (a0 >> 2)], d32 + w);
+        else
+            d32[w] = l32[w - (a0 >> 2)];
+    }
     if (lane < a0 - g0) dst[g0 + lane] = lds[g0 + lane - base];
     if (lane < g1 - a1) dst[a1 + lane] = lds[a1 + lane - base];
 }
