@@ -23,7 +23,14 @@ typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 
 // ---------------------------------------------------------------- rehydrate --
 
-template <bool EXACT>
+// A block takes QB queries at a time (64 while the grid has room for that
+// many blocks, else kBlock): its first QB threads look them up (one lane
+// each) into LDS, then all kBlock threads rebuild the output rows, up to
+// kRehydU (query, 16-byte chunk) tasks per thread with their codebook-row
+// loads issued together, two stages at a time.
+constexpr int kRehydU = 2;
+
+template <int QB, bool EXACT>
 __global__ __launch_bounds__(kBlock) void rehydrate_kernel(
     const double2* __restrict__ pts, const uint32_t* __restrict__ q_stream,
     const uint32_t* __restrict__ q_token, const _Float16* __restrict__ books,
@@ -33,60 +40,107 @@ __global__ __launch_bounds__(kBlock) void rehydrate_kernel(
 {
     extern __shared__ __align__(16) uint8_t lds[];
     const int N = cd.N;
+    // the first batch's query ids load while the tables are staged; each
+    // batch loads the next one's
+    int64_t qs_n = 0, qt_n = 0;
+    {
+        const int64_t q0 = (int64_t)blockIdx.x * QB + threadIdx.x;
+        if (threadIdx.x < QB && q0 < n_q) {
+            qs_n = q_stream[q0];
+            qt_n = q_token[q0];
+        }
+    }
     Tables t = stage_tables(gtab, N, lds, false, EXACT);
     // After the tables: each query of the current batch's book id (-1: no
     // output) and its packed symbols.
     int32_t* qbook = (int32_t*)(lds + staged_table_bytes(N, false, EXACT));
-    uint64_t* qsym = (uint64_t*)(lds + staged_table_bytes(N, false, EXACT) + kBlock * sizeof(int32_t));
+    uint64_t* qsym = (uint64_t*)(lds + staged_table_bytes(N, false, EXACT) + QB * sizeof(int32_t));
     __syncthreads();
     const int64_t n_tok = n_sym / S;
     const int nch = d / 8;   // 16-byte chunks per output row
-    for (int64_t base = (int64_t)blockIdx.x * kBlock; base < n_q; base += (int64_t)gridDim.x * kBlock) {
-        const int64_t q = base + threadIdx.x;
-        int status = 0;
-        uint64_t got = 0;
-        int32_t b = -1;
-        if (q < n_q) {
-            const int64_t s = q_stream[q];
-            const int64_t tk = q_token[q];
-            if (s >= n_streams || tk >= n_tok) {
-                status = 2;
-            } else {
-                status = lookup_token<EXACT>(pts, t, cd, s, tk, S, n_sym, n_spans, false,
-                                             make_double2(0.0, 0.0), &got);
-                if (status == 0) {
-                    b = stream_book[s];
-                    if (b < 0 || b >= n_books) status = 3;
-                    for (int k = 0; k < S; ++k)
-                        if ((int)((got >> (8 * k)) & 0xff) >= K) status = 3;
-                }
+    for (int64_t base = (int64_t)blockIdx.x * QB; base < n_q; base += (int64_t)gridDim.x * QB) {
+        if (threadIdx.x < QB) {
+            const int64_t q = base + threadIdx.x;
+            const int64_t s = qs_n, tk = qt_n;
+            const int64_t qn = q + (int64_t)gridDim.x * QB;
+            if (qn < n_q) {
+                qs_n = q_stream[qn];
+                qt_n = q_token[qn];
             }
-            if (q_status) q_status[q] = (uint8_t)status;
+            int status = 0;
+            uint64_t got = 0;
+            int32_t b = -1;
+            if (q < n_q) {
+                if (s >= n_streams || tk >= n_tok) {
+                    status = 2;
+                } else {
+                    b = stream_book[s];   // loads beside the point
+                    status = lookup_token<EXACT>(pts, t, cd, s, tk, S, n_sym, n_spans, false,
+                                                 make_double2(0.0, 0.0), &got);
+                    if (status == 0) {
+                        if (b < 0 || b >= n_books) status = 3;
+                        for (int k = 0; k < S; ++k)
+                            if ((int)((got >> (8 * k)) & 0xff) >= K) status = 3;
+                    }
+                }
+                if (q_status) q_status[q] = (uint8_t)status;
+            }
+            count_flags(status != 0, n_failed);
+            qbook[threadIdx.x] = status == 0 ? b : -1;
+            qsym[threadIdx.x] = got;
         }
-        count_flags(status != 0, n_failed);
-        qbook[threadIdx.x] = status == 0 ? b : -1;
-        qsym[threadIdx.x] = got;
         __syncthreads();
-        const int nq = (int)min((int64_t)kBlock, n_q - base);
-        for (int task = threadIdx.x; task < nq * nch; task += kBlock) {
-            const int ql = task / nch, ch = task - ql * nch;
-            const int32_t bb = qbook[ql];
-            const uint64_t sy = qsym[ql];
-            double acc[8];
+        const int nq = (int)min((int64_t)QB, n_q - base);
+        const int n_tasks = nq * nch;
+        for (int t0 = threadIdx.x; t0 < n_tasks; t0 += kRehydU * kBlock) {
+            int ql[kRehydU], ch[kRehydU];
+            int32_t bb[kRehydU];
+            uint64_t sy[kRehydU];
+            double acc[kRehydU][8];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) acc[e] = 0.0;
-            if (bb >= 0) {
-                for (int k = 0; k < S; ++k) {
-                    const int i = (int)((sy >> (8 * k)) & 0xff);
-                    const half8 v = *(const half8*)(books + (((int64_t)bb * S + k) * K + i) * d + ch * 8);
+            for (int u = 0; u < kRehydU; ++u) {
+                const int task = t0 + u * kBlock;
+                ql[u] = task < n_tasks ? task / nch : 0;
+                ch[u] = task - ql[u] * nch;
+                bb[u] = task < n_tasks ? qbook[ql[u]] : -1;
+                sy[u] = qsym[ql[u]];
 #pragma unroll
-                    for (int e = 0; e < 8; ++e) acc[e] = acc[e] + (double)v[e];
+                for (int e = 0; e < 8; ++e) acc[u][e] = 0.0;
+            }
+            // stages k and k + 1: every load first, then the sums in stage order
+            for (int k = 0; k < S; k += 2) {
+                half8 v0[kRehydU], v1[kRehydU];
+#pragma unroll
+                for (int u = 0; u < kRehydU; ++u) {
+                    v0[u] = v1[u] = (half8)(_Float16)0;
+                    if (bb[u] >= 0) {
+                        const _Float16* row = books + ((int64_t)bb[u] * S + k) * K * d + ch[u] * 8;
+                        v0[u] = *(const half8*)(row + (int64_t)((sy[u] >> (8 * k)) & 0xff) * d);
+                        if (k + 1 < S)
+                            v1[u] = *(const half8*)(row + (int64_t)K * d +
+                                                    (int64_t)((sy[u] >> (8 * (k + 1))) & 0xff) * d);
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < kRehydU; ++u)
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) acc[u][e] = acc[u][e] + (double)v0[u][e];
+                if (k + 1 < S) {
+#pragma unroll
+                    for (int u = 0; u < kRehydU; ++u)
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) acc[u][e] = acc[u][e] + (double)v1[u][e];
                 }
             }
-            half8 o;
 #pragma unroll
-            for (int e = 0; e < 8; ++e) o[e] = f64_to_f16(acc[e]);
-            *(half8*)(out + (base + ql) * d + ch * 8) = o;
+            for (int u = 0; u < kRehydU; ++u) {
+                if (t0 + u * kBlock < n_tasks) {
+                    half8 o;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) o[e] = f64_to_f16(acc[u][e]);
+                    *(half8*)(out + (base + ql[u]) * d + ch[u] * 8) = o;
+                }
+            }
         }
         __syncthreads();   // the batch's query table is consumed
     }
@@ -262,20 +316,22 @@ extern "C" int fkv_rehydrate(const fkv_codec* c, const void* dev_table, const do
     if ((stream_book && !aligned(stream_book, 4)) || (n_failed && !aligned(n_failed, 4)))
         return FKV_ERR_INVALID_ARG;
     const int64_t n_spans = (n_sym + c->L - 1) / c->L;
+    const bool small_batches = (n_q + 63) / 64 <= kMaxBlocks;
+    const int qb = small_batches ? 64 : kBlock;
     const size_t shm =
-        staged_table_bytes(c->N, false, needs_exact_sectors(c)) + (size_t)kBlock * (sizeof(int32_t) + sizeof(uint64_t));
-    const int64_t nb = blocks_for((n_q + kBlock - 1) / kBlock);
+        staged_table_bytes(c->N, false, needs_exact_sectors(c)) + (size_t)qb * (sizeof(int32_t) + sizeof(uint64_t));
+    const int64_t nb = blocks_for((n_q + qb - 1) / qb);
     const hipStream_t st = (hipStream_t)stream;
+    auto go = [&](auto kern) {
+        hipLaunchKernelGGL(kern, dim3((unsigned)nb), dim3(kBlock), shm, st, (const double2*)points, q_stream, q_token,
+                           (const _Float16*)books_f16, stream_book, (_Float16*)out_f16, q_status, n_failed,
+                           (const uint8_t*)dev_table, codec_args(c), n_streams, n_sym, n_spans, S, K, d, n_books,
+                           n_q);
+    };
     if (needs_exact_sectors(c))
-        hipLaunchKernelGGL((rehydrate_kernel<true>), dim3((unsigned)nb), dim3(kBlock), shm, st,
-                           (const double2*)points, q_stream, q_token, (const _Float16*)books_f16, stream_book,
-                           (_Float16*)out_f16, q_status, n_failed, (const uint8_t*)dev_table, codec_args(c),
-                           n_streams, n_sym, n_spans, S, K, d, n_books, n_q);
+        small_batches ? go(rehydrate_kernel<64, true>) : go(rehydrate_kernel<kBlock, true>);
     else
-        hipLaunchKernelGGL((rehydrate_kernel<false>), dim3((unsigned)nb), dim3(kBlock), shm, st,
-                           (const double2*)points, q_stream, q_token, (const _Float16*)books_f16, stream_book,
-                           (_Float16*)out_f16, q_status, n_failed, (const uint8_t*)dev_table, codec_args(c),
-                           n_streams, n_sym, n_spans, S, K, d, n_books, n_q);
+        small_batches ? go(rehydrate_kernel<64, false>) : go(rehydrate_kernel<kBlock, false>);
     return launch_status();
 }
 
