@@ -69,6 +69,23 @@ def test_rehydrate_hybrid_values_group(fkv, orc):
     assert not st.any()
 
 
+@pytest.mark.parametrize("nq", [64 * 2048, 64 * 2048 + 1, 200000])
+def test_rehydrate_many_queries(fkv, orc, nq):
+    """Query counts on both sides of the switch from 64-query to 256-query batches (the grid holds at
+    most 2048 blocks), with out-of-range queries mixed in."""
+    cfg = w.CONFIGS["tiny"]
+    x, books, sb, xd, bd, sd, sym, codec, pts = _gpu_archive(fkv, cfg)
+    g = cfg.groups[0]
+    ns, Ta = x.shape[0], cfg.T_arch
+    rng = np.random.default_rng(nq)
+    qs = rng.integers(0, ns, nq).astype(np.uint32)
+    qt = rng.integers(0, Ta, nq).astype(np.uint32)
+    qs[::997] = ns
+    qt[5::1009] = Ta
+    _, st = _check_rehydrate(fkv, orc, g, codec, pts, Ta * g.S, books, sb, bd, sd, qs, qt)
+    assert (st == 2).sum() == len(set(range(0, nq, 997)) | set(range(5, nq, 1009))) and (st == 0).any()
+
+
 def test_rehydrate_status_cases(fkv, orc):
     cfg = w.CONFIGS["tiny"]
     x, books, sb, xd, bd, sd, sym, codec, pts = _gpu_archive(fkv, cfg)
