@@ -146,10 +146,13 @@ __global__ __launch_bounds__(kBlock, 8) void cgr_encode_kernel(
 // Bulk decode with no block barrier after the table staging: a wave decodes
 // 128 consecutive spans of one stream (a wave tile), two per lane walked as
 // independent chains so that the look-ups of one overlap the arithmetic of
-// the other, into its own LDS staging area, and writes them back as aligned
-// dwords (bytes at either end); the points of its next wave tile are loaded
-// while the current one decodes.  Points are read and symbols written with
-// streaming accesses: each is touched once, and the tables stay in LDS.
+// the other.  With 6-symbol spans at an even offset (and no verification,
+// which re-reads the symbols), each lane keeps its chains' symbols in
+// registers and stores them as three 16-bit pairs per span; otherwise they go
+// to the wave's LDS staging area and back out as aligned dwords (bytes at
+// either end).  The points of the next wave tile are loaded while the current
+// one decodes.  Points are read and symbols written with streaming accesses:
+// each is touched once, and the tables stay in LDS.
 constexpr int kDecodeSpl = 2;                  // spans per lane
 constexpr int kDecodeTile = 64 * kDecodeSpl;   // spans per wave tile
 
@@ -210,6 +213,36 @@ __device__ __forceinline__ void walk_two(double& ax, double& ay, double& bx, dou
     }
 }
 
+
+// Two backward walks of 6 steps with each chain's symbols kept in registers as
+// three 16-bit pairs (symbol 2p in the low byte, 2p + 1 in the high byte).
+template <bool EXACT>
+__device__ __forceinline__ void walk_two_regs6(double& ax, double& ay, double& bx, double& by, uint32_t (&pa)[3],
+                                               uint32_t (&pb)[3], const Tables& t, const CodecArgs& cd)
+{
+    uint32_t ha = 0, hb = 0;
+#pragma unroll
+    for (int k = 5; k >= 0; --k) {
+        int ca, cb;
+        if (EXACT) {
+            ca = sector_of<EXACT>(ax, ay, t, cd);
+            cb = sector_of<EXACT>(bx, by, t, cd);
+        } else {
+            sector_fast2(ax, ay, bx, by, t.lut, cd.lut_bias, ca, cb);
+        }
+        if (k & 1) {
+            ha = (uint32_t)ca;
+            hb = (uint32_t)cb;
+        } else {
+            pa[k >> 1] = (ha << 8) | (uint32_t)ca;
+            pb[k >> 1] = (hb << 8) | (uint32_t)cb;
+        }
+        const double2 wa = t.Wr[ca], wb = t.Wr[cb];
+        decode_step(ax, ay, wa, cd.inv_r);
+        decode_step(bx, by, wb, cd.inv_r);
+    }
+}
+
 template <bool EXACT, bool VERIFY>
 __global__ __launch_bounds__(kBlock, 8) void cgr_decode_kernel(
     const double2* __restrict__ pts, uint8_t* __restrict__ sym, uint8_t* __restrict__ span_ok,
@@ -253,10 +286,24 @@ __global__ __launch_bounds__(kBlock, 8) void cgr_decode_kernel(
         uint8_t* my0 = stage + (g0 & 3) + lane * L;
         uint8_t* my1 = my0 + 64 * L;
         bool f0 = false, f1 = false;
+        bool direct = false;   // the tile's symbols already stored
         if (nsp == kDecodeTile && (j0 + kDecodeTile) * L <= n_sym) {
             // every span of the tile is whole: both chains run L steps in lockstep
             double ax = P0.x, ay = P0.y, bx = P1.x, by = P1.y;
-            if (L == 6)   // N = 256 at 0.98 r_N: a fixed length, fully unrolled
+            if (!VERIFY && L == 6 && (g0 & 1) == 0) {
+                // symbols straight from registers to global memory, three
+                // 16-bit stores per span (no LDS staging)
+                uint32_t pa[3], pb[3];
+                walk_two_regs6<EXACT>(ax, ay, bx, by, pa, pb, t, cd);
+                uint16_t* da = (uint16_t*)(sym + g0 + lane * 6);
+                uint16_t* db = (uint16_t*)(sym + g0 + (64 + lane) * 6);
+#pragma unroll
+                for (int q = 0; q < 3; ++q) {
+                    __builtin_nontemporal_store((uint16_t)pa[q], da + q);
+                    __builtin_nontemporal_store((uint16_t)pb[q], db + q);
+                }
+                direct = true;
+            } else if (L == 6)   // N = 256 at 0.98 r_N: a fixed length, fully unrolled
                 walk_two<6, EXACT>(ax, ay, bx, by, my0, my1, L, t, cd);
             else
                 walk_two<0, EXACT>(ax, ay, bx, by, my0, my1, L, t, cd);
@@ -290,7 +337,7 @@ __global__ __launch_bounds__(kBlock, 8) void cgr_decode_kernel(
         // the wave's LDS writes above precede its reads below (a wave's LDS
         // operations are performed in order)
         __builtin_amdgcn_wave_barrier();
-        lds_to_bytes_wave<true>(stage, g0, g1, sym, lane);
+        if (!direct) lds_to_bytes_wave<true>(stage, g0, g1, sym, lane);
         P0 = N0;
         P1 = N1;
     }
