@@ -18,7 +18,10 @@ and replayed (no host launch overhead in the timed region); each kernel's
 average duration comes from a graph of back-to-back launches of that kernel.
 `reference_rates` gives what a library fp16 GEMM and a streaming elementwise
 kernel reach on the same device, and each roofline entry its achieved rate as
-a fraction of that (`frac_of_reference`) beside the datasheet fraction.
+a fraction of that (`frac_of_reference`) beside the datasheet fraction; it also
+gives the rate of the library's matrix-core loop (the assignment's instruction
+back to back from registers), and the matrix-bound entries their fraction of
+it (`frac_of_mfma_loop`).
 """
 from __future__ import annotations
 
@@ -544,12 +547,15 @@ def gpu_checks(fkv, cfg, groups):
     return out
 
 
-def reference_rates(torch):
-    """What plain library kernels reach on this device, as context for the
-    roofline fractions: a dense fp16 GEMM (8192 x 8192 x 8192 through
-    torch.matmul) and a streaming elementwise kernel (torch.add over 1 GiB of
-    fp32: 1 GiB read, 1 GiB written).  Best of a few repetitions, events on the
-    current stream."""
+def reference_rates(torch, fkv=None):
+    """What plain kernels reach on this device, as context for the roofline
+    fractions: a dense fp16 GEMM (8192 x 8192 x 8192 through torch.matmul), a
+    streaming elementwise kernel (torch.add over 1 GiB of fp32: 1 GiB read,
+    1 GiB written) and, when the library is given, its matrix-core loop (the
+    assignment's v_mfma_f32_32x32x16_f16 issued back to back from registers by
+    two waves per SIMD, no memory traffic): the practical ceiling of that
+    instruction under the board's power limit.  Best of a few repetitions,
+    events on the current stream."""
     def best_ms(f, reps=5):
         f()
         torch.cuda.synchronize()
@@ -574,10 +580,23 @@ def reference_rates(torch):
     add_ms = best_ms(lambda: torch.add(x, 1.0, out=y))
     del x, y
     torch.cuda.empty_cache()
-    return {"fp16_gemm_tflops": round(2.0 * n ** 3 / (gemm_ms / 1e3) / 1e12, 1),
-            "fp16_gemm": "torch.matmul 8192^3, fp16 in and out",
-            "stream_gbs": round(2.0 * (1 << 30) / (add_ms / 1e3) / 1e9, 1),
-            "stream": "torch.add over 1 GiB fp32 (read + write)"}
+    res = {"fp16_gemm_tflops": round(2.0 * n ** 3 / (gemm_ms / 1e3) / 1e12, 1),
+           "fp16_gemm": "torch.matmul 8192^3, fp16 in and out",
+           "stream_gbs": round(2.0 * (1 << 30) / (add_ms / 1e3) / 1e9, 1),
+           "stream": "torch.add over 1 GiB fp32 (read + write)"}
+    if fkv is not None:
+        out = torch.empty(1, dtype=torch.float32, device="cuda")
+        blocks, iters = 512, 20000
+        flops = fkv.fkv_diag_mfma_loop(blocks, iters, out=out)[1]
+        const_ms = best_ms(lambda: fkv.fkv_diag_mfma_loop(blocks, iters, out=out))
+        if float(out.item()) != 64.0 * iters:
+            raise RuntimeError("matrix-core loop returned %r, expected %r" % (float(out.item()), 64.0 * iters))
+        loop_ms = best_ms(lambda: fkv.fkv_diag_mfma_loop(blocks, iters, out=out, random_operands=True))
+        res["mfma_loop_tflops"] = round(flops / (loop_ms / 1e3) / 1e12, 1)
+        res["mfma_loop"] = ("fkv_diag_mfma_loop: v_mfma_f32_32x32x16_f16 from registers, %d blocks x 4 waves x "
+                            "4 chains x %d, two pseudo-random operand sets alternating per lane" % (blocks, iters))
+        res["mfma_loop_constant_operands_tflops"] = round(flops / (const_ms / 1e3) / 1e12, 1)
+    return res
 
 
 def main():
@@ -722,14 +741,19 @@ def main():
         "cpu_baseline": None,
     }
     if not args.no_reference_rates:
-        ref = reference_rates(torch)
+        ref = reference_rates(torch, fkv)
         line["reference_rates"] = ref
         # each kernel's achieved rate as a fraction of what the library kernel
-        # of the same kind reaches here
+        # of the same kind reaches here, and matrix-bound ones also as a
+        # fraction of the matrix-core loop
         for n, r in rooflines.items():
             r["frac_of_reference"] = round(r["achieved"] / (ref["fp16_gemm_tflops"] if r["bound"] == "mfma"
                                                             else ref["stream_gbs"]), 4)
+            if r["bound"] == "mfma":
+                r["frac_of_mfma_loop"] = round(r["achieved"] / ref["mfma_loop_tflops"], 4)
         roof["frac_of_reference"] = rooflines[dominant]["frac_of_reference"]
+        if "frac_of_mfma_loop" in rooflines[dominant]:
+            roof["frac_of_mfma_loop"] = rooflines[dominant]["frac_of_mfma_loop"]
     line["gpu_checks"] = gpu_checks(fkv, cfg, groups)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(cfg, groups, args.cpu_streams, args.cpu_tokens, 8, 384)

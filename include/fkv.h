@@ -282,6 +282,26 @@ int fkv_kmeans_update_noalloc(const fkv_rvq_desc* desc, const uint16_t* x_f16, u
                               const int32_t* stream_book, const uint8_t* symbols, int32_t stage,
                               uint32_t* counts_out, void* stream);
 
+/* ---------------------------------------------------------------------------
+ * Measurement aid (not part of the archive path).
+ *
+ * fkv_diag_mfma_loop runs n_blocks blocks of 256 threads; every wave issues
+ * iters rounds of four independent v_mfma_f32_32x32x16_f16 (the instruction
+ * of fkv_rvq_assign) from registers, with no memory traffic, and block 0
+ * writes one accumulator sum to out[0] (device float).  With random_operands
+ * = 0 every operand element is a or b, and out[0] = 4 * 16 * iters * a * b
+ * when that is exact; otherwise each lane alternates between two
+ * pseudo-random operand sets, so that the multiplier inputs change on every
+ * instruction as on real data (a and b are ignored).  The rate of the random
+ * form is the device's practical ceiling for that instruction under its
+ * power limit; fkv_diag_mfma_loop_flops gives the FLOP count of a launch
+ * (2*32*32*16 per instruction).  Errors: FKV_ERR_INVALID_ARG for n_blocks < 1,
+ * iters < 0 or a null or misaligned out.
+ * --------------------------------------------------------------------------- */
+int fkv_diag_mfma_loop(int32_t n_blocks, int32_t iters, int32_t random_operands, float a, float b, float* out,
+                       void* stream);
+double fkv_diag_mfma_loop_flops(int32_t n_blocks, int32_t iters);
+
 /* Static description of a status code. */
 const char* fkv_status_string(int status);
 

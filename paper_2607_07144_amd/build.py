@@ -17,7 +17,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libfkv.so")
 
-SOURCES = ["fkv_codec.cpp", "cgr_kernels.hip", "rvq_kernels.hip", "archive_kernels.hip", "kmeans_kernels.hip"]
+SOURCES = ["fkv_codec.cpp", "cgr_kernels.hip", "rvq_kernels.hip", "archive_kernels.hip", "kmeans_kernels.hip",
+           "diag_kernels.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

@@ -59,6 +59,8 @@ _SIGS = {
     "fkv_kmeans_finalize": ([_i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p], ctypes.c_int),
     "fkv_kmeans_update_noalloc": ([ctypes.POINTER(fkv_rvq_desc), _p, _p, _p, _p, _i32, _p, _p], ctypes.c_int),
     "fkv_kmeans_update_noalloc_bytes": ([_i32, _i32, _i32], _sz),
+    "fkv_diag_mfma_loop": ([_i32, _i32, _i32, ctypes.c_float, ctypes.c_float, _p, _p], ctypes.c_int),
+    "fkv_diag_mfma_loop_flops": ([_i32, _i32], _dbl),
     "fkv_status_string": ([ctypes.c_int], ctypes.c_char_p),
     "fkv_version": ([], ctypes.c_char_p),
 }
@@ -414,6 +416,21 @@ def fkv_kmeans_update_noalloc(x, books, stream_book, t_begin: int, t_end: int, s
     _check(lib.fkv_kmeans_update_noalloc(ctypes.byref(desc), _ptr(x), _ptr(books), _ptr(stream_book), _ptr(symbols),
                                          stage, _ptr(counts), _stream(stream)), "fkv_kmeans_update_noalloc")
     return books
+
+
+def fkv_diag_mfma_loop(n_blocks: int, iters: int, out=None, random_operands: bool = False, a: float = 1.0,
+                       b: float = 1.0, stream=None):
+    """Measurement aid: n_blocks blocks of back-to-back v_mfma_f32_32x32x16_f16 from registers (no memory
+    traffic).  Returns (out, flops): out float32 [1] holds block 0's accumulator sum (4 * 16 * iters * a * b
+    for constant operands when exact), flops the launch's FLOP count.  random_operands alternates two
+    pseudo-random operand sets per lane, as real data would."""
+    torch = _torch()
+    if out is None:
+        out = torch.empty(1, dtype=torch.float32, device="cuda")
+    _need(out, torch.float32, "out")
+    _check(lib.fkv_diag_mfma_loop(n_blocks, iters, 1 if random_operands else 0, a, b, _ptr(out), _stream(stream)),
+           "fkv_diag_mfma_loop")
+    return out, lib.fkv_diag_mfma_loop_flops(n_blocks, iters)
 
 
 def fkv_version() -> str:
