@@ -268,7 +268,9 @@ def next_rows(fkv, cfg, groups, side, replays: int):
 
             def lloyd():
                 for stage in range(S):
-                    fkv.fkv_rvq_assign(gr["x"], bk, gr["sb"], cfg.t_begin, cfg.t_end, symbols=symk)
+                    # the update of `stage` uses the assignment of stages 0..stage only
+                    fkv.fkv_rvq_assign(gr["x"], bk, gr["sb"], cfg.t_begin, cfg.t_end, symbols=symk,
+                                       n_stages=stage + 1)
                     fkv.fkv_kmeans_step(gr["x"], bk, gr["sb"], cfg.t_begin, cfg.t_end, symk, stage, sums=sums,
                                         counts=counts)
 
@@ -287,7 +289,7 @@ def next_rows(fkv, cfg, groups, side, replays: int):
                          "streams": sum(gr["ns"] for gr in groups)},
         "kmeans": {"ms_per_lloyd_iteration": round(res["kmeans"]["s"] * 1e3, 4),
                    "books": res["kmeans"]["books"],
-                   "note": "every stage: assignment, cluster sums, centroid update"},
+                   "note": "every stage s: assignment of stages 0..s, cluster sums, centroid update"},
     }
 
 

@@ -121,6 +121,18 @@ int fkv_rvq_assign(const fkv_rvq_desc* desc, const uint16_t* x_f16, const uint16
                    const int32_t* stream_book, uint8_t* symbols, float* residual,
                    uint32_t* n_bad_streams, void* stream);
 
+/* The first n_stages (1..desc->S) stages of fkv_rvq_assign's assignment, in
+ * the same layout (books [n_books][S][K][d], symbols with stride S): what a
+ * k-means update of stage n_stages-1 needs (Sec. 3 "Setup": the later stages
+ * do not enter it).  Symbol bytes of stages >= n_stages are left as they are
+ * (for an invalid stream all S bytes are set to 0xFF, as fkv_rvq_assign
+ * does); the residual, when requested, is the one after n_stages stages.  The
+ * assigned stages' symbols equal fkv_rvq_assign's.  FKV_ERR_INVALID_ARG for
+ * n_stages outside [1, S]; otherwise as fkv_rvq_assign. */
+int fkv_rvq_assign_stages(const fkv_rvq_desc* desc, int32_t n_stages, const uint16_t* x_f16,
+                          const uint16_t* books_f16, const int32_t* stream_book, uint8_t* symbols,
+                          float* residual, uint32_t* n_bad_streams, void* stream);
+
 /* ---- a2 + a3 fused: assignment and span encode in one kernel --------------
  * Equivalent to fkv_rvq_assign followed by fkv_cgr_encode_spans of its
  * symbols (n_sym = (t_end - t_begin) * S per stream): the same symbols and the

@@ -349,7 +349,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
     const _Float16* __restrict__ x, const _Float16* __restrict__ books,
     const int32_t* __restrict__ stream_book, uint8_t* __restrict__ symbols,
     float* __restrict__ residual, uint32_t* __restrict__ n_bad, int64_t T, int64_t t_begin,
-    int64_t Ta, int S, int K, int Kp, int n_books, int64_t blocks_per_stream, int64_t tpb,
+    int64_t Ta, int S, int NS, int K, int Kp, int n_books, int64_t blocks_per_stream, int64_t tpb,
     double2* __restrict__ points, const double2* __restrict__ vtab, double cr, int cN, int cL, int64_t n_spans)
 {
     using C = Cfg<D>;
@@ -410,7 +410,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
 
     // start the first books' copies; zero the buffers' end pads
     book_to_lds_async<D>(bk, K, Kp, lds, wave, lane);
-    if (NBUF > 1 && S > 1) book_to_lds_async<D>(bk + (size_t)K * D, K, Kp, lds + buf_bytes, wave, lane);
+    if (NBUF > 1 && NS > 1) book_to_lds_async<D>(bk + (size_t)K * D, K, Kp, lds + buf_bytes, wave, lane);
     if (tid < NBUF) *(half8*)(lds + tid * buf_bytes + (size_t)Kp * C::ROW_P) = (half8)(_Float16)0;
 
 #pragma unroll
@@ -430,14 +430,14 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
     const uint32_t fa = (uint32_t)(col * C::ROW_P + hh * 16);
 
     wait_all_and_sync();
-    if (NBUF > 1 && S > 1)
+    if (NBUF > 1 && NS > 1)
         book_bias_rows<D, 2>(lds, lds + buf_bytes, Kp);
     else
         book_bias_rows<D, 1>(lds, lds, Kp);
     __syncthreads();
 
     const int nct = Kp / 32;  // even
-    for (int st = 0; st < S; ++st) {
+    for (int st = 0; st < NS; ++st) {
         const int cur = NBUF > 1 ? (st & 1) : 0;
         const uint8_t* buf = lds + cur * buf_bytes;
         const bool two = st > 0;
@@ -475,7 +475,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
             const uint8_t* crow = buf + (size_t)cw * C::ROW_P + hh * 16;
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) cv[ks] = *(const half8*)(crow + ks * 32);
-            const bool last = st + 1 == S;
+            const bool last = st + 1 == NS;
             if (HILO && st >= 1 && !last) {
                 // r = (hi + lo) - c for st >= 2, (x - c_0) - c_1 for st == 1; split again
 #pragma unroll
@@ -515,13 +515,13 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
                 for (int ks = 0; ks < KS; ++ks) bB[tt][ks] = -cv[ks];
             }
         }
-        if (st + 1 < S && (NBUF == 1 || st >= 1 || st + 2 < S)) {
+        if (st + 1 < NS && (NBUF == 1 || st >= 1 || st + 2 < NS)) {
             // Book pipeline: buffer `cur` is free once every wave is past here.
             wait_all_and_sync();
             if (NBUF == 1) {
                 book_to_lds_async<D>(bk + (size_t)(st + 1) * K * D, K, Kp, lds, wave, lane);
                 wait_all_and_sync();
-            } else if (st + 2 < S) {
+            } else if (st + 2 < NS) {
                 book_to_lds_async<D>(bk + (size_t)(st + 2) * K * D, K, Kp, lds + cur * buf_bytes, wave, lane);
             }
             if (NBUF == 1 || st >= 1) {
@@ -622,7 +622,7 @@ template <int D, bool ENC>
 __global__ __launch_bounds__(Cfg<D>::THREADS, kSmallBlocks) void rvq_small_kernel(
     const _Float16* __restrict__ x, const _Float16* __restrict__ books, const int32_t* __restrict__ stream_book,
     uint8_t* __restrict__ symbols, float* __restrict__ residual, uint32_t* __restrict__ n_bad, int64_t T,
-    int64_t t_begin, int64_t Ta, int S, int K, int Kp, int n_books, int64_t blocks_per_stream, int64_t tpi,
+    int64_t t_begin, int64_t Ta, int S, int NS, int K, int Kp, int n_books, int64_t blocks_per_stream, int64_t tpi,
     int64_t ipb, double2* __restrict__ points, const double2* __restrict__ vtab, double cr, int cN, int cL,
     int64_t n_spans)
 {
@@ -664,10 +664,10 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, kSmallBlocks) void rvq_small_kerne
     uint8_t* sym_l = (uint8_t*)(V_l + 256);   // the block's symbols, token-major from tb0
     if (ENC && tid < 256) V_l[tid] = tid < cN ? vtab[tid] : make_double2(NAN, NAN);
     book_to_lds_async<D>(bk, K, Kp, lds, wave, lane);
-    if (S > 1) book_to_lds_async<D>(bk + (size_t)K * D, K, Kp, lds + buf_bytes, wave, lane);
+    if (NS > 1) book_to_lds_async<D>(bk + (size_t)K * D, K, Kp, lds + buf_bytes, wave, lane);
     if (tid < 2) *(half8*)(lds + tid * buf_bytes + (size_t)Kp * C::ROW_P) = (half8)(_Float16)0;
     wait_all_and_sync();
-    if (S > 1)
+    if (NS > 1)
         book_bias_rows<D, 2>(lds, lds + buf_bytes, Kp);
     else
         book_bias_rows<D, 1>(lds, lds, Kp);
@@ -698,7 +698,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, kSmallBlocks) void rvq_small_kerne
         n2 += __uint_as_float(lane_xor32(__float_as_uint(n2), hh));
         bz[0] = bias_column(0.5f * n2 * (1.0f + 0x1p-10f), hh);
 
-        for (int st = 0; st < S; ++st) {
+        for (int st = 0; st < NS; ++st) {
             const uint8_t* buf = lds + st * buf_bytes;
             uint32_t bkey[1] = {0xFFFFFFFFu};
             int bpair[1] = {0};
@@ -725,7 +725,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, kSmallBlocks) void rvq_small_kerne
             const uint8_t* crow = buf + (size_t)cw * C::ROW_P + hh * 16;
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) cv[ks] = *(const half8*)(crow + ks * 32);
-            const bool last = st + 1 == S;
+            const bool last = st + 1 == NS;
             if (last && residual && valid) {
                 float* out = residual + (s * Ta + tok) * D + 8 * hh;
 #pragma unroll
@@ -791,7 +791,7 @@ struct EncArgs {
 };
 
 template <int D, bool HILO, bool ENC>
-int launch_rvq_t(const fkv_rvq_desc* dsc, const uint16_t* x, const uint16_t* books,
+int launch_rvq_t(const fkv_rvq_desc* dsc, int ns, const uint16_t* x, const uint16_t* books,
                  const int32_t* stream_book, uint8_t* symbols, float* residual, uint32_t* n_bad,
                  const EncArgs& enc, hipStream_t stream)
 {
@@ -824,7 +824,7 @@ int launch_rvq_t(const fkv_rvq_desc* dsc, const uint16_t* x, const uint16_t* boo
     const size_t shm = lds_bytes<D>(Kp) + (ENC ? enc_lds_bytes<D>() : 0);
     hipLaunchKernelGGL((rvq_assign_kernel<D, HILO, ENC>), dim3((unsigned)nblk), dim3(Cfg<D>::THREADS), shm, stream,
                        (const _Float16*)x, (const _Float16*)books, stream_book, symbols, residual, n_bad, dsc->T,
-                       dsc->t_begin, Ta, dsc->S, dsc->K, Kp, dsc->n_books, bps, tpb, enc.points, enc.vtab, enc.r,
+                       dsc->t_begin, Ta, dsc->S, ns, dsc->K, Kp, dsc->n_books, bps, tpb, enc.points, enc.vtab, enc.r,
                        enc.N, enc.L, n_spans);
     return launch_status();
 }
@@ -833,7 +833,7 @@ int launch_rvq_t(const fkv_rvq_desc* dsc, const uint16_t* x, const uint16_t* boo
 // wave set, several per block, blocks balanced within a stream so that the
 // grid is about four rounds of resident blocks.
 template <int D, bool ENC>
-int launch_rvq_small(const fkv_rvq_desc* dsc, const uint16_t* x, const uint16_t* books,
+int launch_rvq_small(const fkv_rvq_desc* dsc, int ns, const uint16_t* x, const uint16_t* books,
                      const int32_t* stream_book, uint8_t* symbols, float* residual, uint32_t* n_bad,
                      const EncArgs& enc, hipStream_t stream)
 {
@@ -863,34 +863,36 @@ int launch_rvq_small(const fkv_rvq_desc* dsc, const uint16_t* x, const uint16_t*
     const size_t shm = 2 * buf_bytes_of(Cfg<D>::ROW_P, Kp) + (ENC ? 256 * 16 + (size_t)kSmallMaxItems * TOK * 2 : 0);
     hipLaunchKernelGGL((rvq_small_kernel<D, ENC>), dim3((unsigned)nblk), dim3(Cfg<D>::THREADS), shm, stream,
                        (const _Float16*)x, (const _Float16*)books, stream_book, symbols, residual, n_bad, dsc->T,
-                       dsc->t_begin, Ta, dsc->S, dsc->K, Kp, dsc->n_books, bps, tpi, ipb, enc.points, enc.vtab, enc.r,
+                       dsc->t_begin, Ta, dsc->S, ns, dsc->K, Kp, dsc->n_books, bps, tpi, ipb, enc.points, enc.vtab, enc.r,
                        enc.N, enc.L, n_spans);
     return launch_status();
 }
 
 template <int D>
-int launch_rvq(const fkv_rvq_desc* dsc, const uint16_t* x, const uint16_t* books,
+int launch_rvq(const fkv_rvq_desc* dsc, int ns, const uint16_t* x, const uint16_t* books,
                const int32_t* stream_book, uint8_t* symbols, float* residual, uint32_t* n_bad,
                const EncArgs& enc, hipStream_t stream)
 {
+    // ns stages are assigned (the first ns of the S in the layout); the hi/lo
+    // residual is needed only from a third stage on
     if constexpr (D <= 64) {
-        if (dsc->K <= kSmallK && dsc->S <= 2) {
+        if (dsc->K <= kSmallK && ns <= 2) {
             if (enc.points)
-                return launch_rvq_small<D, true>(dsc, x, books, stream_book, symbols, residual, n_bad, enc, stream);
-            return launch_rvq_small<D, false>(dsc, x, books, stream_book, symbols, residual, n_bad, enc, stream);
+                return launch_rvq_small<D, true>(dsc, ns, x, books, stream_book, symbols, residual, n_bad, enc, stream);
+            return launch_rvq_small<D, false>(dsc, ns, x, books, stream_book, symbols, residual, n_bad, enc, stream);
         }
     }
     if (enc.points) {
-        if (dsc->S <= 2)
-            return launch_rvq_t<D, false, true>(dsc, x, books, stream_book, symbols, residual, n_bad, enc, stream);
-        return launch_rvq_t<D, true, true>(dsc, x, books, stream_book, symbols, residual, n_bad, enc, stream);
+        if (ns <= 2)
+            return launch_rvq_t<D, false, true>(dsc, ns, x, books, stream_book, symbols, residual, n_bad, enc, stream);
+        return launch_rvq_t<D, true, true>(dsc, ns, x, books, stream_book, symbols, residual, n_bad, enc, stream);
     }
-    if (dsc->S <= 2)
-        return launch_rvq_t<D, false, false>(dsc, x, books, stream_book, symbols, residual, n_bad, enc, stream);
-    return launch_rvq_t<D, true, false>(dsc, x, books, stream_book, symbols, residual, n_bad, enc, stream);
+    if (ns <= 2)
+        return launch_rvq_t<D, false, false>(dsc, ns, x, books, stream_book, symbols, residual, n_bad, enc, stream);
+    return launch_rvq_t<D, true, false>(dsc, ns, x, books, stream_book, symbols, residual, n_bad, enc, stream);
 }
 
-int rvq_dispatch(const fkv_rvq_desc* desc, const uint16_t* x_f16, const uint16_t* books_f16,
+int rvq_dispatch(const fkv_rvq_desc* desc, int ns, const uint16_t* x_f16, const uint16_t* books_f16,
                  const int32_t* stream_book, uint8_t* symbols, float* residual, uint32_t* n_bad_streams,
                  const EncArgs& enc, void* stream)
 {
@@ -900,6 +902,7 @@ int rvq_dispatch(const fkv_rvq_desc* desc, const uint16_t* x_f16, const uint16_t
         return FKV_ERR_INVALID_ARG;
     if (d.d < 16 || d.d > 256 || d.d % 16 != 0) return FKV_ERR_INVALID_ARG;
     if (d.S < 1 || d.S > 8 || d.K < 1 || d.K > 256 || d.n_books < 1) return FKV_ERR_INVALID_ARG;
+    if (ns < 1 || ns > d.S || (enc.points && ns != d.S)) return FKV_ERR_INVALID_ARG;
     if (d.n_streams == 0 || d.t_end == d.t_begin) return FKV_OK;
     if (!x_f16 || !books_f16 || !stream_book || !symbols) return FKV_ERR_INVALID_ARG;
     if (!aligned(x_f16, 16) || !aligned(books_f16, 16) || !aligned(stream_book, 4))
@@ -908,7 +911,7 @@ int rvq_dispatch(const fkv_rvq_desc* desc, const uint16_t* x_f16, const uint16_t
     if (n_bad_streams && !aligned(n_bad_streams, 4)) return FKV_ERR_INVALID_ARG;
     const hipStream_t st = (hipStream_t)stream;
 #define FKV_RVQ_CASE(DD) \
-    case DD: return launch_rvq<DD>(desc, x_f16, books_f16, stream_book, symbols, residual, n_bad_streams, enc, st);
+    case DD: return launch_rvq<DD>(desc, ns, x_f16, books_f16, stream_book, symbols, residual, n_bad_streams, enc, st);
     switch (d.d) {
         FKV_RVQ_CASE(16) FKV_RVQ_CASE(32) FKV_RVQ_CASE(48) FKV_RVQ_CASE(64)
         FKV_RVQ_CASE(80) FKV_RVQ_CASE(96) FKV_RVQ_CASE(112) FKV_RVQ_CASE(128)
@@ -929,7 +932,17 @@ extern "C" int fkv_rvq_assign(const fkv_rvq_desc* desc, const uint16_t* x_f16, c
                               uint32_t* n_bad_streams, void* stream)
 {
     const EncArgs none = {nullptr, nullptr, 0.0, 0, 1};
-    return rvq_dispatch(desc, x_f16, books_f16, stream_book, symbols, residual, n_bad_streams, none, stream);
+    return rvq_dispatch(desc, desc ? desc->S : 0, x_f16, books_f16, stream_book, symbols, residual, n_bad_streams,
+                        none, stream);
+}
+
+extern "C" int fkv_rvq_assign_stages(const fkv_rvq_desc* desc, int32_t n_stages, const uint16_t* x_f16,
+                                     const uint16_t* books_f16, const int32_t* stream_book, uint8_t* symbols,
+                                     float* residual, uint32_t* n_bad_streams, void* stream)
+{
+    const EncArgs none = {nullptr, nullptr, 0.0, 0, 1};
+    return rvq_dispatch(desc, n_stages, x_f16, books_f16, stream_book, symbols, residual, n_bad_streams, none,
+                        stream);
 }
 
 extern "C" int fkv_rvq_assign_encode(const fkv_rvq_desc* desc, const uint16_t* x_f16, const uint16_t* books_f16,
@@ -943,5 +956,6 @@ extern "C" int fkv_rvq_assign_encode(const fkv_rvq_desc* desc, const uint16_t* x
     if (!dev_table || !points || !aligned(dev_table, 16) || !aligned(points, 16)) return FKV_ERR_INVALID_ARG;
     const EncArgs enc = {(double2*)points, (const double2*)((const uint8_t*)dev_table + table_off_V(c->N)), c->r,
                          c->N, c->L};
-    return rvq_dispatch(desc, x_f16, books_f16, stream_book, symbols, residual, n_bad_streams, enc, stream);
+    return rvq_dispatch(desc, desc ? desc->S : 0, x_f16, books_f16, stream_book, symbols, residual, n_bad_streams,
+                        enc, stream);
 }

@@ -45,6 +45,7 @@ _SIGS = {
     "fkv_codec_fill_table": ([_PC, _p], ctypes.c_int),
     "fkv_num_spans": ([_PC, _i64], _i64),
     "fkv_rvq_assign": ([ctypes.POINTER(fkv_rvq_desc), _p, _p, _p, _p, _p, _p, _p], ctypes.c_int),
+    "fkv_rvq_assign_stages": ([ctypes.POINTER(fkv_rvq_desc), _i32, _p, _p, _p, _p, _p, _p, _p], ctypes.c_int),
     "fkv_rvq_assign_encode": ([ctypes.POINTER(fkv_rvq_desc), _p, _p, _p, _PC, _p, _p, _p, _p, _p, _p],
                               ctypes.c_int),
     "fkv_cgr_encode_spans": ([_PC, _p, _p, _i64, _i64, _p, _p], ctypes.c_int),
@@ -141,9 +142,11 @@ def fkv_codec_init(N: int, r_scale: float = 0.98, L_override: int = 0) -> Codec:
 # ------------------------------------------------------------------ a2: residual VQ
 
 def fkv_rvq_assign(x, books, stream_book, t_begin: int, t_end: int, symbols=None, residual=None,
-                   want_residual: bool = False, n_bad=None, stream=None):
+                   want_residual: bool = False, n_bad=None, n_stages=None, stream=None):
     """x f16 [n_streams][T][d], books f16 [n_books][S][K][d], stream_book i32 [n_streams] (all CUDA).
-    Returns (symbols u8 [n_streams][(t_end-t_begin)*S], residual f32 or None)."""
+    Returns (symbols u8 [n_streams][(t_end-t_begin)*S], residual f32 or None).  With n_stages (1..S),
+    only the first n_stages stages are assigned (fkv_rvq_assign_stages): the other symbol bytes are left
+    as they are and the residual is the one after n_stages stages."""
     torch = _torch()
     _need(x, torch.float16, "x")
     _need(books, torch.float16, "books")
@@ -167,8 +170,13 @@ def fkv_rvq_assign(x, books, stream_book, t_begin: int, t_end: int, symbols=None
     if n_bad is not None:
         _need(n_bad, torch.int32, "n_bad")
     desc = fkv_rvq_desc(ns, T, t_begin, t_end, d, S, K, nb)
-    _check(lib.fkv_rvq_assign(ctypes.byref(desc), _ptr(x), _ptr(books), _ptr(stream_book), _ptr(symbols),
-                              _ptr(residual), _ptr(n_bad), _stream(stream)), "fkv_rvq_assign")
+    if n_stages is None:
+        _check(lib.fkv_rvq_assign(ctypes.byref(desc), _ptr(x), _ptr(books), _ptr(stream_book), _ptr(symbols),
+                                  _ptr(residual), _ptr(n_bad), _stream(stream)), "fkv_rvq_assign")
+    else:
+        _check(lib.fkv_rvq_assign_stages(ctypes.byref(desc), n_stages, _ptr(x), _ptr(books), _ptr(stream_book),
+                                         _ptr(symbols), _ptr(residual), _ptr(n_bad), _stream(stream)),
+               "fkv_rvq_assign_stages")
     return symbols, residual
 
 

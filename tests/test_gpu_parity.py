@@ -235,6 +235,44 @@ def test_rvq_exact_codeword_inputs_and_duplicates(fkv, orc):
     rvq_check(fkv, orc, x, books, np.zeros(1, np.int32), 0, 300)
 
 
+@pytest.mark.parametrize("d,S,K,T,t0,t1", [
+    (128, 3, 256, 300, 4, 268), (64, 2, 256, 200, 0, 200), (64, 4, 256, 130, 2, 128), (64, 2, 64, 700, 4, 668),
+    (48, 3, 40, 90, 0, 90), (256, 3, 256, 70, 2, 70), (32, 8, 33, 129, 1, 128),
+])
+def test_rvq_assign_first_stages(fkv, d, S, K, T, t0, t1):
+    """fkv_rvq_assign_stages: the assigned stages equal the full assignment's symbols bit for bit, the
+    later stages' bytes are left as they were, an invalid stream gets 0xFF in every stage, and the residual
+    is the one after the assigned stages (x minus their codewords)."""
+    rng = np.random.default_rng(d + 3 * S + K)
+    ns, nb = 4, 2
+    x = (rng.standard_normal((ns, T, d)) * 2).astype(np.float16)
+    books = (rng.standard_normal((nb, S, K, d)) * (0.5 ** np.arange(S))[None, :, None, None]).astype(np.float16)
+    sb = np.array([0, 1, 7, 1], np.int32)          # stream 2 has no book
+    xd, bd, sd = dev(x), dev(books), dev(sb)
+    full, _ = fkv.fkv_rvq_assign(xd, bd, sd, t0, t1)
+    full = host(full).reshape(ns, t1 - t0, S)
+    for n in range(1, S + 1):
+        sym = torch.full((ns, (t1 - t0) * S), 0xA5, dtype=torch.uint8, device="cuda")
+        nbad = torch.zeros(1, dtype=torch.int32, device="cuda")
+        _, res = fkv.fkv_rvq_assign(xd, bd, sd, t0, t1, symbols=sym, want_residual=True, n_bad=nbad, n_stages=n)
+        got = host(sym).reshape(ns, t1 - t0, S)
+        ok = sb < nb
+        assert np.array_equal(got[ok][:, :, :n], full[ok][:, :, :n]), n
+        assert (got[ok][:, :, n:] == 0xA5).all(), n
+        assert (got[~ok] == 0xFF).all() and int(host(nbad)[0]) == 1
+        r = host(res)
+        for si in np.nonzero(ok)[0]:
+            want = x[si, t0:t1].astype(np.float64)
+            for st in range(n):
+                want = want - books[sb[si], st][full[si, :, st]].astype(np.float64)
+            assert np.allclose(r[si], want, rtol=0, atol=1e-5 * (1 + np.abs(want).max())), (n, si)
+        assert np.isnan(r[~ok]).all()
+    with pytest.raises(fkv.FkvError):
+        fkv.fkv_rvq_assign(xd, bd, sd, t0, t1, n_stages=0)
+    with pytest.raises(fkv.FkvError):
+        fkv.fkv_rvq_assign(xd, bd, sd, t0, t1, n_stages=S + 1)
+
+
 def test_rvq_invalid_book_id_is_flagged(fkv):
     rng = np.random.default_rng(4)
     x = rng.standard_normal((3, 70, 64)).astype(np.float16)
