@@ -616,6 +616,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-read-stress", action="store_true",
                     help="skip the read-side measurements on the 144 x 131,072-token archive")
+    ap.add_argument("--no-next-rows", action="store_true",
+                    help="skip rehydrate, eviction and k-means (the rows beyond the step)")
     ap.add_argument("--no-other-workloads", action="store_true",
                     help="skip the GPT-2-shaped and hybrid workloads measured beside the headline one")
     ap.add_argument("--no-reference-rates", action="store_true",
@@ -683,7 +685,7 @@ def main():
         torch.cuda.synchronize()
         phase_ms[n] = e0.elapsed_time(e1) / (reps * max(1, args.steps // 4))
 
-    extra = next_rows(fkv, cfg, groups, side, max(1, args.steps // 4))
+    extra = {} if args.no_next_rows else next_rows(fkv, cfg, groups, side, max(1, args.steps // 4))
     if not args.no_read_stress:
         extra["read_stress"] = read_stress(fkv, side, max(1, args.steps // 4), not args.no_cpu_baseline)
     others_res = None
