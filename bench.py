@@ -227,10 +227,11 @@ def other_workloads(fkv, side, names, n_lookups: int, steps: int, warmup: int, c
     return out
 
 
-def next_rows(fkv, cfg, groups, side, replays: int):
-    """Measurements of the rows beyond the step: rehydration of the step's lookup queries, and one
+def next_rows(fkv, cfg, groups, side, replays: int, cpu: bool = False):
+    """Measurements of the rows beyond the step: rehydration of the step's lookup queries, one
     decoding step's archive update (the position leaving the recent window is assigned on every
-    stream and its symbols appended)."""
+    stream and its symbols appended) and one Lloyd iteration of codebook training.  With `cpu`, the
+    oracle is timed on a bounded sample of each and checks the GPU's results there."""
     import torch
 
     res = {"rehydrate": {"queries": 0, "bytes": 0, "s": 0.0}, "evict_append": {"s": 0.0, "bytes": 0}}
@@ -279,7 +280,9 @@ def next_rows(fkv, cfg, groups, side, replays: int):
             res["kmeans"]["books"] += nb
     rh, ev = res["rehydrate"], res["evict_append"]
     ach = rh["bytes"] / rh["s"] / 1e9
+    cpu_res = next_rows_oracle(fkv, cfg, groups[0]) if cpu else None
     return {
+        "cpu_oracle": cpu_res,
         "rehydrate": {"queries": rh["queries"], "avg_launch_us": round(rh["s"] / len(groups) * 1e6, 2),
                       "queries_per_s": round(rh["queries"] / rh["s"], 1),
                       "roofline": {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
@@ -291,6 +294,80 @@ def next_rows(fkv, cfg, groups, side, replays: int):
                    "books": res["kmeans"]["books"],
                    "note": "every stage s: assignment of stages 0..s, cluster sums, centroid update"},
     }
+
+
+def next_rows_oracle(fkv, cfg, gr):
+    """The oracle on this host for the rows beyond the step, each on a bounded sample of the first
+    group and scaled to the whole workload, and as checker of the GPU's results on that sample:
+    rehydration of the step's queries (outputs rounded once to binary16, statuses), the eviction
+    step on 64 streams (teacher-forced assignment, appended points bit for bit against a fresh GPU
+    append), and a stage-0 Lloyd update on the streams of the first 16 books over their first 1536
+    archived tokens (new codewords bit for bit against the GPU's update of the same sample)."""
+    import torch
+    import oracle
+
+    g = gr["g"]
+    S, L, ns, n_sym = g.S, gr["codec"].L, gr["ns"], gr["n_sym"]
+    threads = oracle.default_threads()
+    oc = oracle.Codec(g.N, g.r_scale)
+    books_h = gr["books"].cpu().numpy()
+    sb_h = gr["sb"].cpu().numpy()
+    pts_h = gr["pts"].cpu().numpy()
+    out = {"cores": threads, "cpu_model": cpu_model(), "kind": "oracle"}
+
+    # rehydration of the step's queries
+    nq = gr["qs"].numel()
+    gout = fkv.fkv_rehydrate(gr["codec"], gr["pts"], n_sym, S, gr["books"], gr["sb"], gr["qs"], gr["qt"])
+    t0 = time.perf_counter()
+    want, wst, _ = oracle.rehydrate(oc, pts_h, n_sym, S, books_h, sb_h, gr["qs_h"].astype(np.uint32),
+                                    gr["qt_h"].astype(np.uint32), threads=threads)
+    t1 = time.perf_counter()
+    out["rehydrate"] = {"queries": nq, "queries_per_s": round(nq / (t1 - t0), 1),
+                        "output_mismatches": int((want.astype(np.float16).view(np.uint16) !=
+                                                  gout.cpu().numpy().view(np.uint16)).any(axis=1).sum()),
+                        "status_nonzero": int((wst != 0).sum())}
+
+    # the eviction step on the first 64 streams: assignment of token t_end - 1, then append
+    n_s = min(64, ns)
+    n_old = n_sym - S
+    sym1 = torch.empty((ns, S), dtype=torch.uint8, device="cuda")
+    fkv.fkv_rvq_assign(gr["x"], gr["books"], gr["sb"], cfg.t_end - 1, cfg.t_end, symbols=sym1)
+    pts2 = gr["pts"].clone()
+    fkv.fkv_cgr_append(gr["codec"], pts2, n_old, sym1)
+    sym1_h = sym1.cpu().numpy()
+    x1 = gr["x"][:n_s, cfg.t_end - 1:cfg.t_end].cpu().numpy()
+    t0 = time.perf_counter()
+    ra = oracle.rvq_assign(x1, books_h, sb_h[:n_s], 0, 1, force=sym1_h[:n_s], want_residual=False,
+                           want_gaps=False, threads=threads)
+    opts = oracle.append(oc, pts_h[:n_s], n_old, ra["symbols"], threads=threads)
+    t1 = time.perf_counter()
+    out["evict_append"] = {"streams": n_s, "us_per_decoding_step": round((t1 - t0) / n_s * ns * 1e6, 1),
+                           "hard_mismatches": ra["n_hard"], "teacher_forced": ra["n_forced"],
+                           "point_mismatches": int((opts.view(np.uint64) !=
+                                                    pts2[:n_s].cpu().numpy().view(np.uint64)).any(axis=2).sum())}
+
+    # a stage-0 Lloyd update on the streams of the first 16 books, first 1536 archived tokens
+    nb_s = min(16, int(books_h.shape[0]))
+    sel = np.nonzero(sb_h < nb_s)[0]
+    te = min(cfg.t_end, cfg.t_begin + 1536)
+    bk_s = gr["books"][:nb_s].clone()
+    symk = torch.empty((ns, (te - cfg.t_begin) * S), dtype=torch.uint8, device="cuda")
+    nbad = torch.zeros(1, dtype=torch.int32, device="cuda")   # the other streams' books are not in the sample
+    fkv.fkv_rvq_assign(gr["x"], bk_s, gr["sb"], cfg.t_begin, te, symbols=symk, n_bad=nbad, n_stages=1)
+    fkv.fkv_kmeans_step(gr["x"], bk_s, gr["sb"], cfg.t_begin, te, symk, 0)
+    xs = gr["x"][torch.from_numpy(sel).cuda(), :te].cpu().numpy()
+    syms = symk.cpu().numpy()[sel]
+    t0 = time.perf_counter()
+    new, _, counts = oracle.kmeans_update(xs, books_h[:nb_s], sb_h[sel], cfg.t_begin, te, syms, 0)
+    t1 = time.perf_counter()
+    tok = len(sel) * (te - cfg.t_begin)
+    out["kmeans_stage0_update"] = {
+        "sample": "%d streams (books 0..%d) x first %d archived tokens" % (len(sel), nb_s - 1, te - cfg.t_begin),
+        "ms_per_stage_update_whole_workload": round((t1 - t0) / tok * ns * (cfg.t_end - cfg.t_begin) * 1e3, 1),
+        "codeword_mismatches": int((new[:, 0].view(np.uint16) != bk_s[:, 0].cpu().numpy().view(np.uint16))
+                                   .any(axis=2).sum()),
+        "members": int(counts.sum())}
+    return out
 
 
 def read_stress(fkv, side, replays: int, cpu: bool = False):
@@ -368,9 +445,22 @@ def read_stress(fkv, side, replays: int, cpu: bool = False):
         lout, lst, _ = oracle.lookup(oc, lpts, n_sym, c["S"], oq[0], oq[1], threads=threads)
         t4 = time.perf_counter()
         gpts = pts[:n_s].cpu().numpy()
+        # the retrieval index of the first 16 streams and one suffix scan over it (hits within those streams)
+        t5 = time.perf_counter()
+        otraj = oracle.trajectory(oc, sym_h[:n_s], codec.L, threads=threads)
+        t6 = time.perf_counter()
+        oh, onh, _ = oracle.suffix_search(oc, otraj, query.cpu().numpy(), verify=True, max_hits=1 << 16)
+        t7 = time.perf_counter()
+        # a fresh GPU scan (the timed replays accumulate into one hit counter)
+        gh_t, gnh, _ = fkv.fkv_suffix_search(codec, traj, query, max_hits=1 << 16)
+        gh = gh_t[:int(gnh.item())].cpu().numpy()
+        gh = gh[gh[:, 0] < n_s]
         cpu_res = {"cores": threads, "cpu_model": cpu_model(), "kind": "oracle",
-                   "sample": "encode and bulk decode of the first %d of %d streams, lookups of the first %d of %d "
-                             "queries, scaled to the whole archive" % (n_s, ns, nq, qs_h.size),
+                   "sample": "encode, bulk decode, index build and one suffix scan of the first %d of %d streams, "
+                             "lookups of the first %d of %d queries, scaled to the whole archive"
+                             % (n_s, ns, nq, qs_h.size),
+                   "index_positions_per_s": round(n_s * n_sym / (t6 - t5), 1),
+                   "suffix_scan_positions_per_s": round(n_s * n_sym / (t7 - t6), 1),
                    "encode_symbols_per_s": round(n_s * n_sym / (t1 - t0), 1),
                    "decode_symbols_per_s": round(n_s * n_sym / (t2 - t1), 1),
                    "lookups_per_s": round(nq / (t4 - t3), 1),
@@ -378,7 +468,12 @@ def read_stress(fkv, side, replays: int, cpu: bool = False):
                               "oracle_decode_failed_spans": int(onf),
                               "decode_symbol_mismatches": int((odec != dec[:n_s].cpu().numpy()).sum()),
                               "lookup_mismatches": int((lout != out[:nq].cpu().numpy()).any(axis=1).sum()),
-                              "lookup_status_nonzero": int((lst != 0).sum())}}
+                              "lookup_status_nonzero": int((lst != 0).sum()),
+                              "index_mismatches": int((otraj.view(np.uint64) !=
+                                                       traj[:n_s].cpu().numpy().view(np.uint64)).any(axis=2).sum()),
+                              "suffix_hits": int(onh),
+                              "suffix_hit_set_equal": sorted(map(tuple, oh.astype(np.int64).tolist())) ==
+                                                      sorted(map(tuple, gh.astype(np.int64).tolist()))}}
     return {
         "archive": "%d streams x %d symbols, N=%d, L=%d" % (ns, n_sym, c["N"], L),
         "cpu_oracle": cpu_res,
@@ -685,7 +780,8 @@ def main():
         torch.cuda.synchronize()
         phase_ms[n] = e0.elapsed_time(e1) / (reps * max(1, args.steps // 4))
 
-    extra = {} if args.no_next_rows else next_rows(fkv, cfg, groups, side, max(1, args.steps // 4))
+    extra = {} if args.no_next_rows else next_rows(fkv, cfg, groups, side, max(1, args.steps // 4),
+                                                   not args.no_cpu_baseline)
     if not args.no_read_stress:
         extra["read_stress"] = read_stress(fkv, side, max(1, args.steps // 4), not args.no_cpu_baseline)
     others_res = None
