@@ -399,6 +399,12 @@ extern "C" int fkv_cgr_encode_spans(const fkv_codec* c, const void* dev_table, c
     if (n_streams == 0 || n_sym == 0) return FKV_OK;
     if (!symbols || !points || !aligned(dev_table, 16) || !aligned(points, 16) || !aligned(symbols, 4))
         return FKV_ERR_INVALID_ARG;
+    if (n_sym % c->L == 0) {
+        // whole spans: the streams sit back to back in both arrays, so they
+        // are tiled as one run of spans (no partial tile at each stream's end)
+        n_sym *= n_streams;
+        n_streams = 1;
+    }
     const int64_t n_spans = (n_sym + c->L - 1) / c->L;
     if (c->L <= 16) {
         const int64_t wtps = (n_spans + kEncTile - 1) / kEncTile;
@@ -428,6 +434,13 @@ extern "C" int fkv_cgr_decode_spans(const fkv_codec* c, const void* dev_table, c
     if (!symbols || !points || !aligned(dev_table, 16) || !aligned(points, 16) || !aligned(symbols, 4))
         return FKV_ERR_INVALID_ARG;
     if (n_failed && !aligned(n_failed, 4)) return FKV_ERR_INVALID_ARG;
+    if (n_sym % c->L == 0) {
+        // whole spans: the streams sit back to back in all three arrays, so
+        // they are tiled as one run of spans (no partial tile at each stream's
+        // end, which would take the per-span path)
+        n_sym *= n_streams;
+        n_streams = 1;
+    }
     const int64_t n_spans = (n_sym + c->L - 1) / c->L;
     const int64_t wtps = (n_spans + kDecodeTile - 1) / kDecodeTile;
     const int64_t n_wtiles = wtps * n_streams;

@@ -56,6 +56,31 @@ def test_encode_decode_parity(fkv, orc, N, scale, Lo):
             assert host(ok).all() and int(host(nf)[0]) == 0
 
 
+@pytest.mark.parametrize("N,n_streams,spans", [(256, 7, 129), (256, 3, 64), (64, 5, 300), (16, 4, 33), (3, 2, 700)])
+def test_whole_span_streams(fkv, orc, N, n_streams, spans):
+    """Streams of whole spans are encoded and decoded as one run of spans (the streams sit back to back in
+    every array), so wave tiles straddle stream boundaries; points, symbols, span flags and the failure
+    count match the oracle, with a corrupted point in a straddling tile."""
+    c, o = fkv.Codec(N), orc.Codec(N)
+    rng = np.random.default_rng(N + n_streams + spans)
+    n_sym = spans * c.L
+    sym = rng.integers(0, N, size=(n_streams, n_sym), dtype=np.uint8)
+    pts = fkv.fkv_cgr_encode_spans(c, dev(sym))
+    want = orc.encode(o, sym)
+    assert host(pts).view(np.uint64).tobytes() == want.view(np.uint64).tobytes()
+    bad = want.copy()
+    bad[min(1, n_streams - 1), spans - 1, 0] += 1e-3       # the last span of a stream
+    bad[0, 0] = (2.0, 2.0)
+    for verify in (False, True):
+        osym, ook, onf, _ = orc.decode(o, bad, n_sym, verify=verify)
+        ok = torch.zeros(ook.shape, dtype=torch.uint8, device="cuda")
+        nf = torch.zeros(1, dtype=torch.int32, device="cuda")
+        dec = host(fkv.fkv_cgr_decode_spans(c, dev(bad), n_sym, span_ok=ok, n_failed=nf, verify=verify))
+        assert np.array_equal(host(ok), ook) and int(host(nf)[0]) == onf == 2
+        good = np.repeat(ook.astype(bool), c.L, axis=1)
+        assert np.array_equal(dec[good], osym[good]) and np.array_equal(dec[good], sym[good])
+
+
 @pytest.mark.parametrize("N", [3, 4, 8, 16, 64, 256])
 def test_constant_spans_every_vertex_direction(fkv, orc, N):
     """Spans of one repeated symbol put the stored point, and every point of its backward walk,
