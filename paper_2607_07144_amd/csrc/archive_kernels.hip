@@ -190,6 +190,10 @@ __global__ __launch_bounds__(kBlock) void append_kernel(double2* __restrict__ pt
 // candidate, kept when decoding ell symbols backward from it reproduces the
 // query.  The scan streams the index once (16 bytes per position).
 
+// WC > 0: the window length is WC, known at compile time, and full windows
+// are walked fully unrolled (the first WC - 1 positions of a stream, with
+// shorter windows, take the loop).
+template <int WC>
 __global__ __launch_bounds__(kBlock) void trajectory_kernel(const uint8_t* __restrict__ sym,
                                                              double2* __restrict__ traj,
                                                              const uint8_t* __restrict__ gtab, CodecArgs cd,
@@ -215,10 +219,20 @@ __global__ __launch_bounds__(kBlock) void trajectory_kernel(const uint8_t* __res
         __syncthreads();
         const int64_t k = k0 + threadIdx.x;
         if (k < k1) {
-            const int64_t a = max((int64_t)0, k - W + 1);
-            const uint8_t* my = tile + (g0 & 3) + (a - a0);
+            const int Wn = WC > 0 ? WC : W;
+            const int64_t a = max((int64_t)0, k - Wn + 1);
+            const uint8_t* my = tile + (g0 & 3) + (int)(a - a0);
+            const int len = (int)(k - a) + 1;
             double px = 0.0, py = 0.0;
-            for (int64_t j = 0; j <= k - a; ++j) encode_step(px, py, V[my[j]], cd.r);
+            if (WC > 0 && len == WC) {
+                double2 v[WC > 0 ? WC : 1];
+#pragma unroll
+                for (int u = 0; u < WC; ++u) v[u] = V[my[u]];
+#pragma unroll
+                for (int u = 0; u < WC; ++u) encode_step(px, py, v[u], cd.r);
+            } else {
+                for (int j = 0; j < len; ++j) encode_step(px, py, V[my[j]], cd.r);
+            }
             store_point_stream(traj + s * n_sym + k, px, py);
         }
     }
@@ -361,9 +375,19 @@ extern "C" int fkv_trajectory(const fkv_codec* c, const void* dev_table, const u
     const int64_t tps = (n_sym + kBlock - 1) / kBlock;
     const int64_t n_tiles = tps * n_streams;
     const size_t shm = 256 * 16 + (size_t)kBlock + 64 + 16;
-    hipLaunchKernelGGL(trajectory_kernel, dim3((unsigned)blocks_for(n_tiles)), dim3(kBlock), shm,
-                       (hipStream_t)stream, symbols, (double2*)traj, (const uint8_t*)dev_table, codec_args(c), n_sym,
-                       W, tps, n_tiles);
+    // the codec's own span length L is the usual window: 6, 9 and 16 for N = 256, 64 and 16
+    auto go = [&](auto kern) {
+        hipLaunchKernelGGL(kern, dim3((unsigned)blocks_for(n_tiles)), dim3(kBlock), shm, (hipStream_t)stream, symbols,
+                           (double2*)traj, (const uint8_t*)dev_table, codec_args(c), n_sym, W, tps, n_tiles);
+    };
+    if (W == 6)
+        go(trajectory_kernel<6>);
+    else if (W == 9)
+        go(trajectory_kernel<9>);
+    else if (W == 16)
+        go(trajectory_kernel<16>);
+    else
+        go(trajectory_kernel<0>);
     return launch_status();
 }
 
