@@ -99,6 +99,11 @@ __device__ __forceinline__ void span_dwords(const uint8_t* __restrict__ sym, con
     for (int c = 0; c < 4; ++c) e[c] = __builtin_amdgcn_alignbyte(dw[c + 1], dw[c], off);
 }
 
+// LC > 0: the span length is LC, known at compile time; a lane whose four
+// spans are all whole walks them fully unrolled with no per-step predicate, so
+// the four chains' steps interleave (the predicated walk puts each chain's
+// step in its own branch region).
+template <int LC>
 __global__ __launch_bounds__(kBlock, 8) void cgr_encode_kernel(
     const uint8_t* __restrict__ sym, double2* __restrict__ pts, const uint8_t* __restrict__ gtab,
     CodecArgs cd, int64_t n_sym, int64_t n_spans, int64_t wtiles_per_stream, int64_t n_wtiles, int64_t total_bytes)
@@ -130,11 +135,22 @@ __global__ __launch_bounds__(kBlock, 8) void cgr_encode_kernel(
         double px[kEncSpl], py[kEncSpl];
 #pragma unroll
         for (int h = 0; h < kEncSpl; ++h) px[h] = py[h] = 0.0;
+        bool whole = LC > 0;
 #pragma unroll
-        for (int k = 0; k < 16; ++k)
+        for (int h = 0; h < kEncSpl; ++h) whole = whole && len[h] == LC;
+        if (whole) {
 #pragma unroll
-            for (int h = 0; h < kEncSpl; ++h)
-                if (k < len[h]) encode_step(px[h], py[h], V[(e[h][k >> 2] >> (8 * (k & 3))) & 0xFF], cd.r);
+            for (int k = 0; k < (LC > 0 ? LC : 1); ++k)
+#pragma unroll
+                for (int h = 0; h < kEncSpl; ++h)
+                    encode_step(px[h], py[h], V[(e[h][k >> 2] >> (8 * (k & 3))) & 0xFF], cd.r);
+        } else {
+#pragma unroll
+            for (int k = 0; k < 16; ++k)
+#pragma unroll
+                for (int h = 0; h < kEncSpl; ++h)
+                    if (k < len[h]) encode_step(px[h], py[h], V[(e[h][k >> 2] >> (8 * (k & 3))) & 0xFF], cd.r);
+        }
 #pragma unroll
         for (int h = 0; h < kEncSpl; ++h)
             if (len[h] > 0) store_point_stream(pts + w.s * n_spans + jj[h], px[h], py[h]);
@@ -410,9 +426,19 @@ extern "C" int fkv_cgr_encode_spans(const fkv_codec* c, const void* dev_table, c
         const int64_t wtps = (n_spans + kEncTile - 1) / kEncTile;
         const int64_t n_wtiles = wtps * n_streams;
         const int64_t nb = min((int64_t)kMaxBlocks, (n_wtiles + kBlock / 64 - 1) / (kBlock / 64));
-        hipLaunchKernelGGL(cgr_encode_kernel, dim3((unsigned)nb), dim3(kBlock), 0, (hipStream_t)stream, symbols,
-                           (double2*)points, (const uint8_t*)dev_table, codec_args(c), n_sym, n_spans, wtps,
-                           n_wtiles, n_streams * n_sym);
+        auto go = [&](auto kern) {
+            hipLaunchKernelGGL(kern, dim3((unsigned)nb), dim3(kBlock), 0, (hipStream_t)stream, symbols,
+                               (double2*)points, (const uint8_t*)dev_table, codec_args(c), n_sym, n_spans, wtps,
+                               n_wtiles, n_streams * n_sym);
+        };
+        if (c->L == 6)   // N = 256, 64 and 16 at 0.98 r_N
+            go(cgr_encode_kernel<6>);
+        else if (c->L == 9)
+            go(cgr_encode_kernel<9>);
+        else if (c->L == 16)
+            go(cgr_encode_kernel<16>);
+        else
+            go(cgr_encode_kernel<0>);
         return launch_status();
     }
     const int64_t tps = (n_spans + kBlock - 1) / kBlock;
