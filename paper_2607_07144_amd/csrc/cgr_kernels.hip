@@ -319,8 +319,12 @@ __global__ __launch_bounds__(kBlock, 8) void cgr_decode_kernel(
                     __builtin_nontemporal_store((uint16_t)pb[q], db + q);
                 }
                 direct = true;
-            } else if (L == 6)   // N = 256 at 0.98 r_N: a fixed length, fully unrolled
+            } else if (L == 6)   // N = 256, 64 and 16 at 0.98 r_N: fixed lengths, fully unrolled
                 walk_two<6, EXACT>(ax, ay, bx, by, my0, my1, L, t, cd);
+            else if (!EXACT && !VERIFY && L == 9)   // (unrolled, the checking instances would spill)
+                walk_two<9, EXACT>(ax, ay, bx, by, my0, my1, L, t, cd);
+            else if (!EXACT && !VERIFY && L == 16)
+                walk_two<16, EXACT>(ax, ay, bx, by, my0, my1, L, t, cd);
             else
                 walk_two<0, EXACT>(ax, ay, bx, by, my0, my1, L, t, cd);
             f0 = !decode_finish<EXACT, VERIFY>(ax, ay, P0, my0, L, t, cd);
