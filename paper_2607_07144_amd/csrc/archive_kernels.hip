@@ -264,13 +264,24 @@ __global__ __launch_bounds__(kBlock) void suffix_search_kernel(
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     const int64_t n_iter = (total + stride - 1) / stride;   // same trip count for every lane
     const int lane = threadIdx.x & 63;
+    // (stream, position) of this thread's index entry, advanced by the grid
+    // stride with additions only: the stride is ds streams and dk < n_sym
+    // positions
+    const int64_t i0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t ds = stride / n_sym, dk = stride - ds * n_sym;
+    int64_t s = i0 / n_sym, k = i0 - s * n_sym;
     for (int64_t it = 0; it < n_iter; ++it) {
-        const int64_t i = it * stride + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+        const int64_t i = it * stride + i0;
+        if (it > 0) {
+            s += ds;
+            k += dk;
+            if (k >= n_sym) {
+                k -= n_sym;
+                ++s;
+            }
+        }
         bool cand = false, hit = false;
-        int64_t s = 0, k = 0;
         if (i < total) {
-            s = i / n_sym;
-            k = i - s * n_sym;
             if (qok && k >= ell - 1) {
                 const double2 p = load_point_stream(traj + i);
                 const double dx = p.x - qx, dy = p.y - qy;
