@@ -161,17 +161,24 @@ def algorithmic(cfg, groups):
     return a
 
 
-def time_graph(fn, reps: int, replays: int, stream):
+def time_graph(fn, reps: int, replays: int, stream, settle_s: float = 0.2):
     """Average duration of one fn() call: a graph of `reps` back-to-back calls, replayed and
-    bracketed by events on the stream the replays run on."""
+    bracketed by events on the stream the replays run on.  Before timing, the graph is replayed
+    for at least `settle_s` seconds, so that the call is timed in its own steady state: after a
+    phase at the board's power limit (the assignment) the shader clock takes a while to recover,
+    and a kernel timed right after it would carry that phase's clock."""
     import torch
 
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g, stream=stream):
         for _ in range(reps):
             fn()
+    t0 = time.perf_counter()
     g.replay()
     torch.cuda.synchronize()
+    while time.perf_counter() - t0 < settle_s:
+        g.replay()
+        torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     for _ in range(replays):
