@@ -769,7 +769,9 @@ def main():
     ms_step = start.elapsed_time(stop) / args.steps
 
     # Average duration of each kernel: a graph of `reps` back-to-back launches of
-    # that kernel alone, replayed and bracketed by events on the launch stream.
+    # that kernel alone, replayed for at least 0.2 s (the kernel's own steady
+    # state; see time_graph), then replayed and bracketed by events on the
+    # launch stream.
     reps = 10
     phase_ms = {}
     for n in names:
@@ -777,8 +779,12 @@ def main():
         with torch.cuda.graph(g, stream=side):
             for _ in range(reps):
                 run_kernel(fkv, cfg, groups, n)
+        t_settle = time.perf_counter()
         g.replay()
         torch.cuda.synchronize()
+        while time.perf_counter() - t_settle < 0.2:
+            g.replay()
+            torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()  # replay() launches on the current stream
         for _ in range(max(1, args.steps // 4)):
