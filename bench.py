@@ -161,7 +161,10 @@ def algorithmic(cfg, groups):
     return a
 
 
-def time_graph(fn, reps: int, replays: int, stream, settle_s: float = 0.2):
+SETTLE_S = 0.2   # --settle-s
+
+
+def time_graph(fn, reps: int, replays: int, stream, settle_s: float | None = None):
     """Average duration of one fn() call: a graph of `reps` back-to-back calls, replayed and
     bracketed by events on the stream the replays run on.  Before timing, the graph is replayed
     for at least `settle_s` seconds, so that the call is timed in its own steady state: after a
@@ -169,6 +172,8 @@ def time_graph(fn, reps: int, replays: int, stream, settle_s: float = 0.2):
     and a kernel timed right after it would carry that phase's clock."""
     import torch
 
+    if settle_s is None:
+        settle_s = SETTLE_S
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g, stream=stream):
         for _ in range(reps):
@@ -724,11 +729,16 @@ def main():
                     help="skip the GPT-2-shaped and hybrid workloads measured beside the headline one")
     ap.add_argument("--no-reference-rates", action="store_true",
                     help="skip the library GEMM and streaming-kernel reference rates")
+    ap.add_argument("--settle-s", type=float, default=0.2,
+                    help="seconds each timing graph is replayed before it is timed (0: no settle period; "
+                         "counter passes, which need few dispatches, use 0)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="also run one streaming elementwise kernel (torch.neg) that reads and writes "
                          "this many MiB before the step: a kernel of known traffic for scaling HBM "
                          "byte counters")
     args = ap.parse_args()
+    global SETTLE_S
+    SETTLE_S = args.settle_s
     if args.gpus != 1:
         print("bench.py measures the path on one GPU; it has no multi-GPU mode (the streams are "
               "independent and would shard across GPUs with no exchange)", file=sys.stderr)
@@ -782,7 +792,7 @@ def main():
         t_settle = time.perf_counter()
         g.replay()
         torch.cuda.synchronize()
-        while time.perf_counter() - t_settle < 0.2:
+        while time.perf_counter() - t_settle < SETTLE_S:
             g.replay()
             torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
