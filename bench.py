@@ -260,18 +260,23 @@ def next_rows(fkv, cfg, groups, side, replays: int, cpu: bool = False):
             res["rehydrate"]["queries"] += nq
             res["rehydrate"]["bytes"] += nq * (8 + g.S * cfg.d * 2 + cfg.d * 2) + 16 * spans
             res["rehydrate"]["s"] += t
-            # one eviction: token t_end - 1 of every stream, appended after the archived symbols
+            # one eviction: token t_end - 1 of every stream, appended after the archived symbols; the
+            # assignment takes the streams of each book together (one block per book's streams)
             ns = gr["ns"]
             n_old = gr["n_sym"] - g.S
             pts = gr["pts"].clone()
             sym1 = torch.empty((ns, g.S), dtype=torch.uint8, device="cuda")
+            grp = torch.from_numpy(fkv.book_groups(gr["sb"].cpu().numpy())).cuda()
 
             def step():
-                fkv.fkv_rvq_assign(gr["x"], gr["books"], gr["sb"], cfg.t_end - 1, cfg.t_end, symbols=sym1)
+                fkv.fkv_rvq_assign_groups(gr["x"], gr["books"], gr["sb"], grp, cfg.t_end - 1, cfg.t_end,
+                                          symbols=sym1)
                 fkv.fkv_cgr_append(gr["codec"], pts, n_old, sym1)
 
             res["evict_append"]["s"] += time_graph(step, 10, replays, side)
             res["evict_append"]["bytes"] += ns * (cfg.d * 2 + g.S) + gr["books"].numel() * 2 + ns * 32
+            res["evict_append"]["groups"] = res["evict_append"].get("groups", 0) + int(grp.shape[0])
+            res["evict_append"]["group_size"] = int(grp.shape[1])
             # one Lloyd iteration of codebook training over every stage (assign, accumulate, update)
             bk = gr["books"].clone()
             nb, S, K = bk.shape[0], bk.shape[1], bk.shape[2]
@@ -301,7 +306,8 @@ def next_rows(fkv, cfg, groups, side, replays: int, cpu: bool = False):
                                    "frac": round(ach / PEAK_HBM_GBS, 4)}},
         "evict_append": {"us_per_decoding_step": round(ev["s"] * 1e6, 2),
                          "positions_per_s": round(1.0 / ev["s"], 1),
-                         "streams": sum(gr["ns"] for gr in groups)},
+                         "streams": sum(gr["ns"] for gr in groups),
+                         "assignment": "grouped by book: %d groups of %d streams" % (ev["groups"], ev["group_size"])},
         "kmeans": {"ms_per_lloyd_iteration": round(res["kmeans"]["s"] * 1e3, 4),
                    "books": res["kmeans"]["books"],
                    "note": "every stage s: assignment of stages 0..s, cluster sums, centroid update"},
@@ -343,7 +349,8 @@ def next_rows_oracle(fkv, cfg, gr):
     n_s = min(64, ns)
     n_old = n_sym - S
     sym1 = torch.empty((ns, S), dtype=torch.uint8, device="cuda")
-    fkv.fkv_rvq_assign(gr["x"], gr["books"], gr["sb"], cfg.t_end - 1, cfg.t_end, symbols=sym1)
+    grp = torch.from_numpy(fkv.book_groups(sb_h)).cuda()
+    fkv.fkv_rvq_assign_groups(gr["x"], gr["books"], gr["sb"], grp, cfg.t_end - 1, cfg.t_end, symbols=sym1)
     pts2 = gr["pts"].clone()
     fkv.fkv_cgr_append(gr["codec"], pts2, n_old, sym1)
     sym1_h = sym1.cpu().numpy()

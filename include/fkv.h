@@ -133,6 +133,33 @@ int fkv_rvq_assign_stages(const fkv_rvq_desc* desc, int32_t n_stages, const uint
                           const uint16_t* books_f16, const int32_t* stream_book, uint8_t* symbols,
                           float* residual, uint32_t* n_bad_streams, void* stream);
 
+/* ---- a2, grouped by book: the per-step eviction form (Sec. 3 "Setup") ------
+ * When a position ages out of the exact window at a decoding step, every
+ * stream's leaving vector is assigned: one token per stream.  A per-stream
+ * block would copy a whole stage book into LDS for that one token, so this
+ * form takes groups of streams that share a book and gives each block the
+ * tokens [t_begin, t_end) of all members of one group (member by member),
+ * served from one copy of the book.  The symbols and residuals of every
+ * listed stream are those fkv_rvq_assign gives, bit for bit (the arithmetic of
+ * a token does not depend on the other tokens of its block); streams not
+ * listed are not touched.
+ *   groups        device int32 [n_groups][group_size] (4-byte aligned):
+ *                 stream ids; all members of a group must have the same book
+ *                 id in stream_book.  A stream listed in two groups is
+ *                 assigned twice (the same bytes are written twice).
+ *   n_groups      >= 0 (0: nothing to do; groups may then be null)
+ *   group_size    1..256
+ * A group with a member id outside [0, n_streams), or whose members' book ids
+ * differ or lie outside [0, n_books): the symbols of its in-range members are
+ * set to 0xFF (residual NaN) and *n_bad_groups (if given) is incremented once
+ * per such group.  The other arguments are those of fkv_rvq_assign; errors as
+ * fkv_rvq_assign, and FKV_ERR_INVALID_ARG for a group_size outside 1..256, a
+ * negative n_groups, or groups null or misaligned with n_groups > 0. */
+int fkv_rvq_assign_groups(const fkv_rvq_desc* desc, const int32_t* groups, int64_t n_groups,
+                          int32_t group_size, const uint16_t* x_f16, const uint16_t* books_f16,
+                          const int32_t* stream_book, uint8_t* symbols, float* residual,
+                          uint32_t* n_bad_groups, void* stream);
+
 /* ---- a2 + a3 fused: assignment and span encode in one kernel --------------
  * Equivalent to fkv_rvq_assign followed by fkv_cgr_encode_spans of its
  * symbols (n_sym = (t_end - t_begin) * S per stream): the same symbols and the

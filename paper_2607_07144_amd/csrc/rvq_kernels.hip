@@ -61,6 +61,7 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 constexpr int kLdsBudget = 160 * 1024;
 constexpr float kBiasHiScale = 16384.0f;   // weight of the bias's second fp16 slot
+constexpr int kMaxGroup = 256;             // streams per group in the grouped form (<= threads per block)
 
 // One LDS book buffer: Kp rows of row_p bytes, then a 16-byte zero pad.
 __host__ __device__ constexpr size_t buf_bytes_of(int row_p, int Kp)
@@ -344,14 +345,20 @@ __device__ __forceinline__ void resplit2(uint32_t a, uint32_t b, uint32_t c, uin
     nb = l;
 }
 
-template <int D, bool HILO, bool ENC>
+// GRP: a work item is a group of G streams that share one book (groups[g * G
+// + e] is member e of group g) and its tokens are the members' archived
+// tokens, member by member, so that one block serves all of them with a single
+// copy of the book (the per-token arithmetic is that of the per-stream form).
+template <int D, bool HILO, bool ENC, bool GRP>
 __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assign_kernel(
     const _Float16* __restrict__ x, const _Float16* __restrict__ books,
     const int32_t* __restrict__ stream_book, uint8_t* __restrict__ symbols,
     float* __restrict__ residual, uint32_t* __restrict__ n_bad, int64_t T, int64_t t_begin,
     int64_t Ta, int S, int NS, int K, int Kp, int n_books, int64_t blocks_per_stream, int64_t tpb,
-    double2* __restrict__ points, const double2* __restrict__ vtab, double cr, int cN, int cL, int64_t n_spans)
+    double2* __restrict__ points, const double2* __restrict__ vtab, double cr, int cN, int cL, int64_t n_spans,
+    const int32_t* __restrict__ groups, int G, int64_t n_streams)
 {
+    static_assert(!(GRP && ENC), "the grouped form has no fused encode");
     using C = Cfg<D>;
     constexpr int KS = C::KS, TT = C::TT, TOK = C::TOK, NBUF = C::NBUF;
     extern __shared__ __align__(16) uint8_t lds[];
@@ -364,33 +371,74 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
     const uint32_t nblk = gridDim.x, q8 = nblk / 8, r8 = nblk % 8;
     const uint32_t xcd = blockIdx.x % 8, slot = blockIdx.x / 8;
     const int64_t item = (int64_t)xcd * q8 + min(xcd, r8) + slot;
-    const int64_t s = item / blocks_per_stream;
+    const int64_t s = item / blocks_per_stream;                // the stream (GRP: the group)
+    const int64_t Tv = GRP ? (int64_t)G * Ta : Ta;             // the item's tokens
     const int64_t tb = (item - s * blocks_per_stream) * tpb;   // first token of the block
-    const int64_t te = min(Ta, tb + tpb);                      // one past its last
+    const int64_t te = min(Tv, tb + tpb);                      // one past its last
 
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int col = lane & 31, hh = lane >> 5;
     uint8_t* sym_s = symbols + s * Ta * S;
-    const int b = stream_book[s];
+    int b = GRP ? -1 : stream_book[s];
 
     // this lane's tokens (independent of the book id, so their loads overlap its)
     int64_t tok[TT];
     bool valid[TT];
+    int64_t srow[TT];               // GRP: the token's row in the [n_streams][Ta] outputs
     half8 bA[TT][KS], bB[TT][KS];   // B operands of the current stage's passes
     half8 bz[TT];                   // bias-step B operand
 #pragma unroll
     for (int tt = 0; tt < TT; ++tt) {
         tok[tt] = tb + (int64_t)(wave * TT + tt) * 32 + col;
         valid[tt] = tok[tt] < te;
-        const _Float16* row = x + (s * T + t_begin + (valid[tt] ? tok[tt] : 0)) * D + 8 * hh;
+        int64_t xr;
+        if constexpr (GRP) {
+            // member e's token t; a member id out of range rejects the group
+            // below, and meanwhile reads stream 0
+            const int64_t tv = valid[tt] ? tok[tt] : tb;
+            const int64_t e = tv / Ta, t = tv - e * Ta;
+            const int64_t m = groups[s * G + e];
+            const int64_t mm = (m >= 0 && m < n_streams) ? m : 0;
+            srow[tt] = mm * Ta + t;
+            xr = mm * T + t_begin + t;
+        } else {
+            srow[tt] = 0;
+            xr = s * T + t_begin + (valid[tt] ? tok[tt] : 0);
+        }
+        const _Float16* row = x + xr * D + 8 * hh;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
             bA[tt][ks] = valid[tt] ? *(const half8*)(row + 16 * ks) : (half8)(_Float16)0;
             bB[tt][ks] = (half8)(_Float16)0;
         }
     }
+    if constexpr (GRP) {
+        // the group's book: its first member's, which every member must share
+        const int32_t m0 = groups[s * G];
+        const int gb = (m0 >= 0 && m0 < n_streams) ? stream_book[m0] : -1;
+        int bad = gb < 0 || gb >= n_books;
+        if (tid < G) {
+            const int32_t m = groups[s * G + tid];
+            bad |= m < 0 || m >= n_streams || stream_book[m] != gb;
+        }
+        b = __syncthreads_or(bad) ? -1 : gb;
+    }
 
     if (b < 0 || b >= n_books) {
+        if constexpr (GRP) {
+            // every in-range member's symbols (and residual) of the block's tokens
+            for (int64_t i = tb * S + tid; i < te * S; i += C::THREADS) {
+                const int64_t j = i / S, e = j / Ta, m = groups[s * G + e];
+                if (m >= 0 && m < n_streams) symbols[(m * Ta + (j - e * Ta)) * S + (i - j * S)] = 0xFF;
+            }
+            if (residual)
+                for (int64_t i = tb * D + tid; i < te * D; i += C::THREADS) {
+                    const int64_t j = i / D, e = j / Ta, m = groups[s * G + e];
+                    if (m >= 0 && m < n_streams) residual[(m * Ta + (j - e * Ta)) * D + (i - j * D)] = NAN;
+                }
+            if (tid == 0 && tb == 0 && n_bad) atomicAdd(n_bad, 1u);
+            return;
+        }
         for (int64_t i = tb * S + tid; i < te * S; i += C::THREADS) sym_s[i] = 0xFF;
         if (ENC)   // the block's spans encode 0xFF symbols: NaN points, as a separate encode gives
             for (int64_t j = tb * S / cL + tid; j < (te * S + cL - 1) / cL; j += C::THREADS)
@@ -437,6 +485,9 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
     __syncthreads();
 
     const int nct = Kp / 32;  // even
+    // GRP: a wave without tokens (short items, such as one token per member)
+    // skips the scans and only takes part in the book pipeline
+    const bool wave_on = !GRP || __builtin_amdgcn_readfirstlane((int)(tb + (int64_t)wave * TT * 32 < te));
     for (int st = 0; st < NS; ++st) {
         const int cur = NBUF > 1 ? (st & 1) : 0;
         const uint8_t* buf = lds + cur * buf_bytes;
@@ -448,6 +499,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
             bkey[tt] = 0xFFFFFFFFu;
             bpair[tt] = 0;
         }
+        if (wave_on) {
         if (two)
             stage_scan<D, TT, true>(buf, fa, nct, bz, bA, bB, bkey, bpair);
         else
@@ -465,7 +517,10 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
                 cw = ocw;
             }
             if (hh == 0 && valid[tt]) {
-                sym_s[tok[tt] * S + st] = (uint8_t)cw;
+                if (GRP)
+                    symbols[srow[tt] * S + st] = (uint8_t)cw;
+                else
+                    sym_s[tok[tt] * S + st] = (uint8_t)cw;
                 if (ENC) sym_l[(tok[tt] - tb) * S + st] = (uint8_t)cw;
             }
             // next stage's bias: this stage's winning |u| grown by 2^-10
@@ -496,7 +551,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
                 }
             }
             if (last && residual && valid[tt]) {
-                float* out = residual + (s * Ta + tok[tt]) * D + 8 * hh;
+                float* out = residual + (GRP ? srow[tt] : s * Ta + tok[tt]) * D + 8 * hh;
 #pragma unroll
                 for (int ks = 0; ks < KS; ++ks) {
                     floatx4 lo4, hi4;
@@ -515,6 +570,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
                 for (int ks = 0; ks < KS; ++ks) bB[tt][ks] = -cv[ks];
             }
         }
+        }   // wave_on
         if (st + 1 < NS && (NBUF == 1 || st >= 1 || st + 2 < NS)) {
             // Book pipeline: buffer `cur` is free once every wave is past here.
             wait_all_and_sync();
@@ -790,15 +846,23 @@ struct EncArgs {
     int N, L;
 };
 
-template <int D, bool HILO, bool ENC>
+// Stream groups of the grouped form (on = false: the per-stream form).
+struct GroupArgs {
+    bool on;
+    const int32_t* groups;
+    int64_t n_groups;
+    int G;
+};
+
+template <int D, bool HILO, bool ENC, bool GRP>
 int launch_rvq_t(const fkv_rvq_desc* dsc, int ns, const uint16_t* x, const uint16_t* books,
                  const int32_t* stream_book, uint8_t* symbols, float* residual, uint32_t* n_bad,
-                 const EncArgs& enc, hipStream_t stream)
+                 const EncArgs& enc, const GroupArgs& grp, hipStream_t stream)
 {
     static std::once_flag once;
     const int Kp = (dsc->K + 63) / 64 * 64;  // whole pairs of 32-codeword tiles
     std::call_once(once, [] {
-        (void)hipFuncSetAttribute((const void*)rvq_assign_kernel<D, HILO, ENC>,
+        (void)hipFuncSetAttribute((const void*)rvq_assign_kernel<D, HILO, ENC, GRP>,
                                   hipFuncAttributeMaxDynamicSharedMemorySize,
                                   (int)(lds_bytes<D>(256) + (ENC ? enc_lds_bytes<D>() : 0)));
     });
@@ -817,15 +881,16 @@ int launch_rvq_t(const fkv_rvq_desc* dsc, int ns, const uint16_t* x, const uint1
         const int unit = enc.L / a;
         tpb = (int64_t)(Cfg<D>::TOK / unit) * unit;
     }
-    const int64_t bps = (Ta + tpb - 1) / tpb;
-    const int64_t nblk = bps * dsc->n_streams;
+    const int64_t items = GRP ? grp.n_groups : dsc->n_streams;
+    const int64_t bps = ((GRP ? grp.G * Ta : Ta) + tpb - 1) / tpb;
+    const int64_t nblk = bps * items;
     if (nblk > 0x7fffffff) return FKV_ERR_UNSUPPORTED;
     const int64_t n_spans = ENC ? (Ta * dsc->S + enc.L - 1) / enc.L : 0;
     const size_t shm = lds_bytes<D>(Kp) + (ENC ? enc_lds_bytes<D>() : 0);
-    hipLaunchKernelGGL((rvq_assign_kernel<D, HILO, ENC>), dim3((unsigned)nblk), dim3(Cfg<D>::THREADS), shm, stream,
-                       (const _Float16*)x, (const _Float16*)books, stream_book, symbols, residual, n_bad, dsc->T,
-                       dsc->t_begin, Ta, dsc->S, ns, dsc->K, Kp, dsc->n_books, bps, tpb, enc.points, enc.vtab, enc.r,
-                       enc.N, enc.L, n_spans);
+    hipLaunchKernelGGL((rvq_assign_kernel<D, HILO, ENC, GRP>), dim3((unsigned)nblk), dim3(Cfg<D>::THREADS), shm,
+                       stream, (const _Float16*)x, (const _Float16*)books, stream_book, symbols, residual, n_bad,
+                       dsc->T, dsc->t_begin, Ta, dsc->S, ns, dsc->K, Kp, dsc->n_books, bps, tpb, enc.points, enc.vtab,
+                       enc.r, enc.N, enc.L, n_spans, grp.groups, grp.G, dsc->n_streams);
     return launch_status();
 }
 
@@ -871,10 +936,17 @@ int launch_rvq_small(const fkv_rvq_desc* dsc, int ns, const uint16_t* x, const u
 template <int D>
 int launch_rvq(const fkv_rvq_desc* dsc, int ns, const uint16_t* x, const uint16_t* books,
                const int32_t* stream_book, uint8_t* symbols, float* residual, uint32_t* n_bad,
-               const EncArgs& enc, hipStream_t stream)
+               const EncArgs& enc, const GroupArgs& grp, hipStream_t stream)
 {
     // ns stages are assigned (the first ns of the S in the layout); the hi/lo
     // residual is needed only from a third stage on
+    if (grp.on) {
+        if (ns <= 2)
+            return launch_rvq_t<D, false, false, true>(dsc, ns, x, books, stream_book, symbols, residual, n_bad, enc,
+                                                       grp, stream);
+        return launch_rvq_t<D, true, false, true>(dsc, ns, x, books, stream_book, symbols, residual, n_bad, enc, grp,
+                                                  stream);
+    }
     if constexpr (D <= 64) {
         if (dsc->K <= kSmallK && ns <= 2) {
             if (enc.points)
@@ -884,17 +956,21 @@ int launch_rvq(const fkv_rvq_desc* dsc, int ns, const uint16_t* x, const uint16_
     }
     if (enc.points) {
         if (ns <= 2)
-            return launch_rvq_t<D, false, true>(dsc, ns, x, books, stream_book, symbols, residual, n_bad, enc, stream);
-        return launch_rvq_t<D, true, true>(dsc, ns, x, books, stream_book, symbols, residual, n_bad, enc, stream);
+            return launch_rvq_t<D, false, true, false>(dsc, ns, x, books, stream_book, symbols, residual, n_bad, enc,
+                                                       grp, stream);
+        return launch_rvq_t<D, true, true, false>(dsc, ns, x, books, stream_book, symbols, residual, n_bad, enc, grp,
+                                                  stream);
     }
     if (ns <= 2)
-        return launch_rvq_t<D, false, false>(dsc, ns, x, books, stream_book, symbols, residual, n_bad, enc, stream);
-    return launch_rvq_t<D, true, false>(dsc, ns, x, books, stream_book, symbols, residual, n_bad, enc, stream);
+        return launch_rvq_t<D, false, false, false>(dsc, ns, x, books, stream_book, symbols, residual, n_bad, enc,
+                                                    grp, stream);
+    return launch_rvq_t<D, true, false, false>(dsc, ns, x, books, stream_book, symbols, residual, n_bad, enc, grp,
+                                               stream);
 }
 
 int rvq_dispatch(const fkv_rvq_desc* desc, int ns, const uint16_t* x_f16, const uint16_t* books_f16,
                  const int32_t* stream_book, uint8_t* symbols, float* residual, uint32_t* n_bad_streams,
-                 const EncArgs& enc, void* stream)
+                 const EncArgs& enc, void* stream, const GroupArgs& grp = GroupArgs{false, nullptr, 0, 0})
 {
     if (!desc) return FKV_ERR_INVALID_ARG;
     const fkv_rvq_desc& d = *desc;
@@ -903,7 +979,9 @@ int rvq_dispatch(const fkv_rvq_desc* desc, int ns, const uint16_t* x_f16, const 
     if (d.d < 16 || d.d > 256 || d.d % 16 != 0) return FKV_ERR_INVALID_ARG;
     if (d.S < 1 || d.S > 8 || d.K < 1 || d.K > 256 || d.n_books < 1) return FKV_ERR_INVALID_ARG;
     if (ns < 1 || ns > d.S || (enc.points && ns != d.S)) return FKV_ERR_INVALID_ARG;
-    if (d.n_streams == 0 || d.t_end == d.t_begin) return FKV_OK;
+    if (grp.on && (grp.n_groups < 0 || grp.G < 1 || grp.G > kMaxGroup || enc.points)) return FKV_ERR_INVALID_ARG;
+    if (grp.on && grp.n_groups > 0 && (!grp.groups || !aligned(grp.groups, 4))) return FKV_ERR_INVALID_ARG;
+    if (d.n_streams == 0 || d.t_end == d.t_begin || (grp.on && grp.n_groups == 0)) return FKV_OK;
     if (!x_f16 || !books_f16 || !stream_book || !symbols) return FKV_ERR_INVALID_ARG;
     if (!aligned(x_f16, 16) || !aligned(books_f16, 16) || !aligned(stream_book, 4))
         return FKV_ERR_INVALID_ARG;
@@ -911,7 +989,7 @@ int rvq_dispatch(const fkv_rvq_desc* desc, int ns, const uint16_t* x_f16, const 
     if (n_bad_streams && !aligned(n_bad_streams, 4)) return FKV_ERR_INVALID_ARG;
     const hipStream_t st = (hipStream_t)stream;
 #define FKV_RVQ_CASE(DD) \
-    case DD: return launch_rvq<DD>(desc, ns, x_f16, books_f16, stream_book, symbols, residual, n_bad_streams, enc, st);
+    case DD: return launch_rvq<DD>(desc, ns, x_f16, books_f16, stream_book, symbols, residual, n_bad_streams, enc, grp, st);
     switch (d.d) {
         FKV_RVQ_CASE(16) FKV_RVQ_CASE(32) FKV_RVQ_CASE(48) FKV_RVQ_CASE(64)
         FKV_RVQ_CASE(80) FKV_RVQ_CASE(96) FKV_RVQ_CASE(112) FKV_RVQ_CASE(128)
@@ -958,4 +1036,15 @@ extern "C" int fkv_rvq_assign_encode(const fkv_rvq_desc* desc, const uint16_t* x
                          c->N, c->L};
     return rvq_dispatch(desc, desc ? desc->S : 0, x_f16, books_f16, stream_book, symbols, residual, n_bad_streams,
                         enc, stream);
+}
+
+extern "C" int fkv_rvq_assign_groups(const fkv_rvq_desc* desc, const int32_t* groups, int64_t n_groups,
+                                     int32_t group_size, const uint16_t* x_f16, const uint16_t* books_f16,
+                                     const int32_t* stream_book, uint8_t* symbols, float* residual,
+                                     uint32_t* n_bad_groups, void* stream)
+{
+    const EncArgs none = {nullptr, nullptr, 0.0, 0, 1};
+    const GroupArgs grp = {true, groups, n_groups, group_size};
+    return rvq_dispatch(desc, desc ? desc->S : 0, x_f16, books_f16, stream_book, symbols, residual, n_bad_groups,
+                        none, stream, grp);
 }

@@ -46,6 +46,8 @@ _SIGS = {
     "fkv_num_spans": ([_PC, _i64], _i64),
     "fkv_rvq_assign": ([ctypes.POINTER(fkv_rvq_desc), _p, _p, _p, _p, _p, _p, _p], ctypes.c_int),
     "fkv_rvq_assign_stages": ([ctypes.POINTER(fkv_rvq_desc), _i32, _p, _p, _p, _p, _p, _p, _p], ctypes.c_int),
+    "fkv_rvq_assign_groups": ([ctypes.POINTER(fkv_rvq_desc), _p, _i64, _i32, _p, _p, _p, _p, _p, _p, _p],
+                              ctypes.c_int),
     "fkv_rvq_assign_encode": ([ctypes.POINTER(fkv_rvq_desc), _p, _p, _p, _PC, _p, _p, _p, _p, _p, _p],
                               ctypes.c_int),
     "fkv_cgr_encode_spans": ([_PC, _p, _p, _i64, _i64, _p, _p], ctypes.c_int),
@@ -177,6 +179,55 @@ def fkv_rvq_assign(x, books, stream_book, t_begin: int, t_end: int, symbols=None
         _check(lib.fkv_rvq_assign_stages(ctypes.byref(desc), n_stages, _ptr(x), _ptr(books), _ptr(stream_book),
                                          _ptr(symbols), _ptr(residual), _ptr(n_bad), _stream(stream)),
                "fkv_rvq_assign_stages")
+    return symbols, residual
+
+
+def book_groups(stream_book) -> "np.ndarray":
+    """Host-side grouping for fkv_rvq_assign_groups: the streams of each book that has any, in stream order,
+    as int32 [n_used_books][members] (every used book must have the same number of streams)."""
+    import numpy as np
+    sb = np.asarray(stream_book).reshape(-1)
+    order = np.argsort(sb, kind="stable")
+    books, counts = np.unique(sb, return_counts=True)
+    if counts.size == 0:
+        return np.zeros((0, 1), np.int32)
+    if (counts != counts[0]).any():
+        raise ValueError("books have different numbers of streams")
+    return order.reshape(books.size, counts[0]).astype(np.int32)
+
+
+def fkv_rvq_assign_groups(x, books, stream_book, groups, t_begin: int, t_end: int, symbols=None, residual=None,
+                          want_residual: bool = False, n_bad=None, stream=None):
+    """fkv_rvq_assign for the streams listed in groups (i32 [n_groups][group_size], CUDA; the members of a
+    group share a book), one block per group's tokens.  Returns (symbols, residual or None) in the layout of
+    fkv_rvq_assign; streams not listed keep their symbol bytes."""
+    torch = _torch()
+    _need(x, torch.float16, "x")
+    _need(books, torch.float16, "books")
+    _need(stream_book, torch.int32, "stream_book")
+    _need(groups, torch.int32, "groups")
+    ns, T, d = x.shape
+    nb, S, K, d2 = books.shape
+    if d2 != d or stream_book.shape != (ns,) or groups.dim() != 2:
+        raise ValueError("shape mismatch between x, books, stream_book and groups")
+    Ta = t_end - t_begin
+    if symbols is None:
+        symbols = torch.empty((ns, Ta * S), dtype=torch.uint8, device=x.device)
+    _need(symbols, torch.uint8, "symbols")
+    if symbols.numel() != ns * Ta * S:
+        raise ValueError("symbols has the wrong size")
+    if residual is None and want_residual:
+        residual = torch.empty((ns, Ta, d), dtype=torch.float32, device=x.device)
+    if residual is not None:
+        _need(residual, torch.float32, "residual")
+        if residual.numel() != ns * Ta * d:
+            raise ValueError("residual has the wrong size")
+    if n_bad is not None:
+        _need(n_bad, torch.int32, "n_bad")
+    desc = fkv_rvq_desc(ns, T, t_begin, t_end, d, S, K, nb)
+    _check(lib.fkv_rvq_assign_groups(ctypes.byref(desc), _ptr(groups), groups.shape[0], groups.shape[1], _ptr(x),
+                                     _ptr(books), _ptr(stream_book), _ptr(symbols), _ptr(residual), _ptr(n_bad),
+                                     _stream(stream)), "fkv_rvq_assign_groups")
     return symbols, residual
 
 

@@ -149,10 +149,11 @@ def test_append_out_of_alphabet_is_nan(fkv):
     assert not np.isnan(p[0, 0]).any() and np.isnan(p[1, 0]).all()
 
 
-def test_eviction_loop_matches_bulk_archive(fkv, orc):
+@pytest.mark.parametrize("grouped", [False, True])
+def test_eviction_loop_matches_bulk_archive(fkv, orc, grouped):
     """A decoding model's archive: each step assigns the position leaving the recent window
-    (all streams at once) and appends its S symbols; after the loop the archive equals a bulk
-    encode of the symbols of every archived position."""
+    (all streams at once; grouped: one block per book's streams) and appends its S symbols; after
+    the loop the archive equals a bulk encode of the symbols of every archived position."""
     cfg = w.CONFIGS["gpt2"]
     g = cfg.groups[0]
     x, books, sb = w.make_group_numpy(cfg)
@@ -165,8 +166,12 @@ def test_eviction_loop_matches_bulk_archive(fkv, orc):
     pts = torch.zeros((ns, cap, 2), dtype=torch.float64, device="cuda")
     pts[:, :codec.n_spans(sym0.shape[1])] = fkv.fkv_cgr_encode_spans(codec, sym0)
     n = sym0.shape[1]
+    gd = torch.from_numpy(fkv.book_groups(sb)).cuda()
     for t in range(start, start + steps):
-        s1, _ = fkv.fkv_rvq_assign(xd, bd, sd, t, t + 1)
+        if grouped:
+            s1, _ = fkv.fkv_rvq_assign_groups(xd, bd, sd, gd, t, t + 1)
+        else:
+            s1, _ = fkv.fkv_rvq_assign(xd, bd, sd, t, t + 1)
         fkv.fkv_cgr_append(codec, pts, n, s1)
         n += g.S
     sym_all, _ = fkv.fkv_rvq_assign(xd, bd, sd, cfg.t_begin, start + steps)
