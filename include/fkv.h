@@ -160,12 +160,17 @@ int fkv_rvq_assign_groups(const fkv_rvq_desc* desc, const int32_t* groups, int64
                           const int32_t* stream_book, uint8_t* symbols, float* residual,
                           uint32_t* n_bad_groups, void* stream);
 
-/* ---- a2 + a3 fused: assignment and span encode in one kernel --------------
+/* ---- a2 + a3 fused: assignment and span encode in one call -----------------
  * Equivalent to fkv_rvq_assign followed by fkv_cgr_encode_spans of its
  * symbols (n_sym = (t_end - t_begin) * S per stream): the same symbols and the
- * same points, bit for bit.  Each assignment block takes a token range that
- * holds whole spans (a multiple of L / gcd(L, S) tokens) and encodes them as
- * soon as its last stage is assigned, so the symbols are never read back.
+ * same points, bit for bit.  Below 2^23 head vectors per call (n_streams x
+ * (t_end - t_begin)), or when symbols is not 4-byte aligned, one kernel does
+ * both: each assignment block takes a token range that holds whole spans (a
+ * multiple of L / gcd(L, S) tokens) and encodes them as soon as its last stage
+ * is assigned, so the symbols are never read back.  From 2^23 head vectors on
+ * the call launches the assignment and then the span encode on the same
+ * stream, which is faster there (the encode tail of a fused block holds its
+ * compute unit; fkv_rvq_assign_encode_fused says which form a call takes).
  *   c, dev_table  the codec, as for fkv_cgr_encode_spans
  *   points        device f64 [n_streams][n_spans][2] (n_spans = ceil(n_sym / L)),
  *                 16-byte aligned; a stream with an invalid book id gets NaN
@@ -175,6 +180,12 @@ int fkv_rvq_assign_encode(const fkv_rvq_desc* desc, const uint16_t* x_f16, const
                           const int32_t* stream_book, const fkv_codec* c, const void* dev_table,
                           uint8_t* symbols, double* points, float* residual, uint32_t* n_bad_streams,
                           void* stream);
+
+/* Which form fkv_rvq_assign_encode takes for this descriptor and symbols
+ * pointer: 1 the single fused kernel, 0 the assignment kernel and then the
+ * span encode kernel.  Host-only (no device call); FKV_ERR_INVALID_ARG for a
+ * null descriptor. */
+int fkv_rvq_assign_encode_fused(const fkv_rvq_desc* desc, const uint8_t* symbols);
 
 /* ---- a3: fixed-span chaos-game encode (Sec. 1 "The code", Sec. 2) --------
  * symbols [n_streams][n_sym] (device u8) -> points [n_streams][n_spans][2]

@@ -1000,10 +1000,31 @@ int rvq_dispatch(const fkv_rvq_desc* desc, int ns, const uint16_t* x_f16, const 
 #undef FKV_RVQ_CASE
 }
 
+// From this many head vectors per call on, fkv_rvq_assign_encode runs the
+// assignment and then the span encode as two kernels.  The fused kernel's
+// encode tail sits on every block's critical path (one block per compute unit
+// at d = 128, so about 1,000 blocks in a row per compute unit at the
+// long-context shape: 0.85 ms more than the separate encode's 0.12 ms);
+// below a few thousand blocks the one launch and the symbols never read back
+// win (GPT-2 shape: 37 us fused against 41 us).
+constexpr int64_t kSplitHeadVectors = (int64_t)1 << 23;
+
+bool encode_split(const fkv_rvq_desc* desc, const uint8_t* symbols)
+{
+    return desc && desc->n_streams > 0 && desc->t_end > desc->t_begin &&
+           desc->n_streams * (desc->t_end - desc->t_begin) >= kSplitHeadVectors && aligned(symbols, 4);
+}
+
 }  // namespace
 }  // namespace fkv
 
 using namespace fkv;
+
+extern "C" int fkv_rvq_assign_encode_fused(const fkv_rvq_desc* desc, const uint8_t* symbols)
+{
+    if (!desc) return FKV_ERR_INVALID_ARG;
+    return encode_split(desc, symbols) ? 0 : 1;
+}
 
 extern "C" int fkv_rvq_assign(const fkv_rvq_desc* desc, const uint16_t* x_f16, const uint16_t* books_f16,
                               const int32_t* stream_book, uint8_t* symbols, float* residual,
@@ -1032,6 +1053,17 @@ extern "C" int fkv_rvq_assign_encode(const fkv_rvq_desc* desc, const uint16_t* x
         !(c->r_max > 0.0 && c->r <= c->r_max * (1.0 + 1e-12)))
         return FKV_ERR_INVALID_ARG;
     if (!dev_table || !points || !aligned(dev_table, 16) || !aligned(points, 16)) return FKV_ERR_INVALID_ARG;
+    if (encode_split(desc, symbols)) {
+        // assignment, then the encode of its symbols on the same stream: the
+        // same symbols and points as the fused kernel, bit for bit (an invalid
+        // stream's 0xFF symbols encode to NaN points there too)
+        const EncArgs none = {nullptr, nullptr, 0.0, 0, 1};
+        const int rc = rvq_dispatch(desc, desc->S, x_f16, books_f16, stream_book, symbols, residual, n_bad_streams,
+                                    none, stream);
+        if (rc != FKV_OK) return rc;
+        return fkv_cgr_encode_spans(c, dev_table, symbols, desc->n_streams, (desc->t_end - desc->t_begin) * desc->S,
+                                    points, stream);
+    }
     const EncArgs enc = {(double2*)points, (const double2*)((const uint8_t*)dev_table + table_off_V(c->N)), c->r,
                          c->N, c->L};
     return rvq_dispatch(desc, desc ? desc->S : 0, x_f16, books_f16, stream_book, symbols, residual, n_bad_streams,

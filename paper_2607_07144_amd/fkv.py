@@ -46,6 +46,7 @@ _SIGS = {
     "fkv_num_spans": ([_PC, _i64], _i64),
     "fkv_rvq_assign": ([ctypes.POINTER(fkv_rvq_desc), _p, _p, _p, _p, _p, _p, _p], ctypes.c_int),
     "fkv_rvq_assign_stages": ([ctypes.POINTER(fkv_rvq_desc), _i32, _p, _p, _p, _p, _p, _p, _p], ctypes.c_int),
+    "fkv_rvq_assign_encode_fused": ([ctypes.POINTER(fkv_rvq_desc), _p], ctypes.c_int),
     "fkv_rvq_assign_groups": ([ctypes.POINTER(fkv_rvq_desc), _p, _i64, _i32, _p, _p, _p, _p, _p, _p, _p],
                               ctypes.c_int),
     "fkv_rvq_assign_encode": ([ctypes.POINTER(fkv_rvq_desc), _p, _p, _p, _PC, _p, _p, _p, _p, _p, _p],
@@ -229,6 +230,19 @@ def fkv_rvq_assign_groups(x, books, stream_book, groups, t_begin: int, t_end: in
                                      _ptr(books), _ptr(stream_book), _ptr(symbols), _ptr(residual), _ptr(n_bad),
                                      _stream(stream)), "fkv_rvq_assign_groups")
     return symbols, residual
+
+
+def fkv_rvq_assign_encode_fused(x, books, t_begin: int, t_end: int, symbols=None) -> bool:
+    """Whether fkv_rvq_assign_encode runs its single fused kernel for these shapes (True) or the assignment
+    and then the span encode (False); symbols is the output tensor the call would get, if any."""
+    ns, T, d = x.shape
+    nb, S, K, _ = books.shape
+    desc = fkv_rvq_desc(ns, T, t_begin, t_end, d, S, K, nb)
+    ptr = _ptr(symbols) if symbols is not None else ctypes.c_void_p(256)   # a fresh tensor is aligned
+    r = lib.fkv_rvq_assign_encode_fused(ctypes.byref(desc), ptr)
+    if r < 0:
+        raise FkvError(r, "fkv_rvq_assign_encode_fused")
+    return r == 1
 
 
 def fkv_rvq_assign_encode(codec: Codec, x, books, stream_book, t_begin: int, t_end: int, symbols=None, points=None,

@@ -333,6 +333,25 @@ def test_invalid_arguments_retrieval_kmeans_fused(F):
     assert fused(codec=F.fkv_codec(2, 6, 0.1, 0.2)) == E
     assert fused(tab=None) == E and fused(pts=None) == E and fused(pts=P(0x10008)) == E
     assert fused(D(4, 100, 4, 101, 64, 2, 256, 4)) == E
+    # the two-kernel form (2^23 head vectors and more) validates on the host as well
+    big = D(2048, 32768, 36, 32768, 128, 3, 256, 512)
+    assert fused(big, codec=too_big) == E and fused(big, pts=None) == E and fused(big, pts=P(0x10008)) == E
+    assert fused(D(2048, 32768, 36, 32768, 120, 3, 256, 512)) == E and fused(D(2048, 32768, 36, 32769, 128, 3, 256, 512)) == E
+    assert fused(D(2048, 32768, 36, 32768, 128, 3, 257, 512)) == E
+
+
+def test_fused_call_form(F):
+    """fkv_rvq_assign_encode runs the fused kernel below 2^23 head vectors per call (or with symbols
+    that are not 4-byte aligned) and the assignment then the encode from there on; the query says which."""
+    lib, D, P = F.lib, F.fkv_rvq_desc, ctypes.c_void_p
+    form = lambda desc, sym=P(0x10000): lib.fkv_rvq_assign_encode_fused(ctypes.byref(desc), sym)
+    assert form(D(2048, 32768, 36, 32768, 128, 3, 256, 512)) == 0        # the long-context step
+    assert form(D(2048, 32768, 36, 32768, 128, 3, 256, 512), P(0x10001)) == 1
+    assert form(D(288, 1024, 4, 992, 64, 2, 256, 144)) == 1             # GPT-2 shape
+    assert form(D(256, 32769, 1, 32769, 64, 2, 256, 1)) == 0            # exactly 2^23
+    assert form(D(256, 32769, 2, 32769, 64, 2, 256, 1)) == 1            # one token per stream fewer
+    assert form(D(0, 32769, 1, 32769, 64, 2, 256, 1)) == 1
+    assert lib.fkv_rvq_assign_encode_fused(None, P(0x10000)) == F.FKV_ERR_INVALID_ARG
 
 
 def test_noalloc_kmeans_rejects_inputs_beyond_its_scratch(F):

@@ -152,3 +152,38 @@ def test_fused_shapes(fkv, d, S, K, N, T):
         assert np.array_equal(np.isnan(a), np.isnan(b))
         a, b = np.nan_to_num(a), np.nan_to_num(b)
     assert np.array_equal(a.view(np.uint64), b.view(np.uint64))
+
+
+@pytest.mark.parametrize("d,S,K,N", [(32, 3, 64, 64), (16, 2, 16, 16)])
+def test_fused_split_form(fkv, d, S, K, N):
+    """From 2^23 head vectors per call the fused entry point runs the assignment and then the span
+    encode; with symbols that are not 4-byte aligned it runs the fused kernel at any size.  Both forms
+    give the same symbols, points (NaN on the stream without a valid book) and residuals.  S = 3 runs the
+    general kernel, S = 2 with K = 16 the small-book one; L = 9 leaves a ragged last span."""
+    rng = np.random.default_rng(d + S)
+    ns, T, t0, t1 = 64, 131076, 2, 131074          # 64 x 131072 = 2^23 head vectors
+    x = torch.from_numpy((rng.standard_normal((ns, T, d)) * 1.5).astype(np.float16)).cuda()
+    books = torch.from_numpy((rng.standard_normal((2, S, K, d)) *
+                              (0.5 ** np.arange(S))[None, :, None, None]).astype(np.float16)).cuda()
+    sbh = rng.integers(0, 2, ns).astype(np.int32)
+    sbh[5] = 9                                      # no valid book
+    sb = torch.from_numpy(sbh).cuda()
+    codec = fkv.Codec(N)
+    n = (t1 - t0) * S
+    assert not fkv.fkv_rvq_assign_encode_fused(x, books, t0, t1)
+    buf = torch.empty(ns * n + 1, dtype=torch.uint8, device="cuda")
+    odd = buf[1:].view(ns, n)                       # not 4-byte aligned: the fused kernel runs
+    assert fkv.fkv_rvq_assign_encode_fused(x, books, t0, t1, symbols=odd)
+    nb1 = torch.zeros(1, dtype=torch.int32, device="cuda")
+    nb2 = torch.zeros(1, dtype=torch.int32, device="cuda")
+    s1, p1, r1 = fkv.fkv_rvq_assign_encode(codec, x, books, sb, t0, t1, want_residual=True, n_bad=nb1)
+    s2, p2, r2 = fkv.fkv_rvq_assign_encode(codec, x, books, sb, t0, t1, symbols=odd, want_residual=True, n_bad=nb2)
+    assert torch.equal(s1, s2) and int(nb1.item()) == int(nb2.item()) == 1
+    a, b = host(p1), host(p2)
+    assert np.array_equal(np.isnan(a), np.isnan(b)) and np.isnan(a[5]).all()
+    assert np.array_equal(np.nan_to_num(a).view(np.uint64), np.nan_to_num(b).view(np.uint64))
+    ra, rb = host(r1), host(r2)
+    assert np.array_equal(np.isnan(ra), np.isnan(rb))
+    assert np.array_equal(np.nan_to_num(ra).view(np.uint32), np.nan_to_num(rb).view(np.uint32))
+    del x, buf, odd, s1, s2, p1, p2, r1, r2
+    torch.cuda.empty_cache()
