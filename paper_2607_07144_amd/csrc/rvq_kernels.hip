@@ -45,6 +45,7 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <type_traits>
 #include <mutex>
 
 #include "fkv.h"
@@ -488,10 +489,15 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
     // GRP: a wave without tokens (short items, such as one token per member)
     // skips the scans and only takes part in the book pipeline
     const bool wave_on = !GRP || __builtin_amdgcn_readfirstlane((int)(tb + (int64_t)wave * TT * 32 < te));
-    for (int st = 0; st < NS; ++st) {
+    // One stage: TWO (stages 1..) scans with two passes per tile.  Stage 0 is
+    // issued on its own, ahead of the loop over the later stages: with one
+    // loop body holding both scan forms the register allocator kept both
+    // forms' values live across the loop and spilled (d = 128, three stages:
+    // 256 VGPRs and 32 bytes of scratch per lane, against 188 and none).
+    auto stage = [&](const int st, auto two_c) {
+        constexpr bool TWO = decltype(two_c)::value;
         const int cur = NBUF > 1 ? (st & 1) : 0;
         const uint8_t* buf = lds + cur * buf_bytes;
-        const bool two = st > 0;
         uint32_t bkey[TT];
         int bpair[TT];
 #pragma unroll
@@ -500,10 +506,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
             bpair[tt] = 0;
         }
         if (wave_on) {
-        if (two)
-            stage_scan<D, TT, true>(buf, fa, nct, bz, bA, bB, bkey, bpair);
-        else
-            stage_scan<D, TT, false>(buf, fa, nct, bz, bA, bB, bkey, bpair);
+        stage_scan<D, TT, TWO>(buf, fa, nct, bz, bA, bB, bkey, bpair);
 #pragma unroll
         for (int tt = 0; tt < TT; ++tt) {
             const int li = (int)(bkey[tt] & 31u);
@@ -531,7 +534,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) cv[ks] = *(const half8*)(crow + ks * 32);
             const bool last = st + 1 == NS;
-            if (HILO && st >= 1 && !last) {
+            if (HILO && TWO && !last) {
                 // r = (hi + lo) - c for st >= 2, (x - c_0) - c_1 for st == 1; split again
 #pragma unroll
                 for (int ks = 0; ks < KS; ++ks) {
@@ -557,7 +560,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
                     floatx4 lo4, hi4;
 #pragma unroll
                     for (int e = 0; e < 8; ++e) {
-                        const float rv = (float)bA[tt][ks][e] + (st > 0 ? (float)bB[tt][ks][e] : 0.0f) -
+                        const float rv = (float)bA[tt][ks][e] + (TWO ? (float)bB[tt][ks][e] : 0.0f) -
                                          (float)cv[ks][e];
                         if (e < 4) lo4[e] = rv; else hi4[e - 4] = rv;
                     }
@@ -565,7 +568,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
                     *(floatx4*)(out + 16 * ks + 4) = hi4;
                 }
             }
-            if (st == 0 && !last) {
+            if (!TWO && !last) {
 #pragma unroll
                 for (int ks = 0; ks < KS; ++ks) bB[tt][ks] = -cv[ks];
             }
@@ -586,7 +589,9 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
             }
             __syncthreads();
         }
-    }
+        };
+    stage(0, std::false_type{});
+    for (int st = 1; st < NS; ++st) stage(st, std::true_type{});
     if (ENC) {
         // Span encode of the block's symbols (Sec. 1 "The code"): the block's
         // token range holds whole spans, each walked from the anchor (0,0) with
@@ -754,14 +759,13 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, kSmallBlocks) void rvq_small_kerne
         n2 += __uint_as_float(lane_xor32(__float_as_uint(n2), hh));
         bz[0] = bias_column(0.5f * n2 * (1.0f + 0x1p-10f), hh);
 
-        for (int st = 0; st < NS; ++st) {
+        // stage 0, then stage 1 (as in rvq_assign_kernel: one body per scan form)
+        auto stage = [&](const int st, auto two_c) {
+            constexpr bool TWO = decltype(two_c)::value;
             const uint8_t* buf = lds + st * buf_bytes;
             uint32_t bkey[1] = {0xFFFFFFFFu};
             int bpair[1] = {0};
-            if (st > 0)
-                stage_scan_small<D, true>(buf, fa, bz, cur, bB, bkey, bpair);
-            else
-                stage_scan_small<D, false>(buf, fa, bz, cur, bB, bkey, bpair);
+            stage_scan_small<D, TWO>(buf, fa, bz, cur, bB, bkey, bpair);
             const int li = (int)(bkey[0] & 31u);
             int cw = (li >> 4) * 32 + 8 * ((li & 15) >> 2) + 4 * hh + (li & 3);
             cw = min(cw, K - 1);  // only reachable with all-NaN scores; keeps reads in bounds
@@ -789,7 +793,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, kSmallBlocks) void rvq_small_kerne
                     floatx4 lo4, hi4;
 #pragma unroll
                     for (int e = 0; e < 8; ++e) {
-                        const float rv = (float)cur[0][ks][e] + (st > 0 ? (float)bB[0][ks][e] : 0.0f) -
+                        const float rv = (float)cur[0][ks][e] + (TWO ? (float)bB[0][ks][e] : 0.0f) -
                                          (float)cv[ks][e];
                         if (e < 4) lo4[e] = rv; else hi4[e - 4] = rv;
                     }
@@ -797,11 +801,13 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, kSmallBlocks) void rvq_small_kerne
                     *(floatx4*)(out + 16 * ks + 4) = hi4;
                 }
             }
-            if (st == 0 && !last) {
+            if (!TWO && !last) {
 #pragma unroll
                 for (int ks = 0; ks < KS; ++ks) bB[0][ks] = -cv[ks];
             }
-        }
+                };
+        stage(0, std::false_type{});
+        if (NS > 1) stage(1, std::true_type{});
     };
     half8 rB[1][KS];
     for (int64_t tb = tb0; tb < te0; tb += 2 * tpi) {
