@@ -506,73 +506,73 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
             bpair[tt] = 0;
         }
         if (wave_on) {
-        stage_scan<D, TT, TWO>(buf, fa, nct, bz, bA, bB, bkey, bpair);
+            stage_scan<D, TT, TWO>(buf, fa, nct, bz, bA, bB, bkey, bpair);
 #pragma unroll
-        for (int tt = 0; tt < TT; ++tt) {
-            const int li = (int)(bkey[tt] & 31u);
-            int cw = (2 * bpair[tt] + (li >> 4)) * 32 + 8 * ((li & 15) >> 2) + 4 * hh + (li & 3);
-            cw = min(cw, K - 1);  // only reachable with all-NaN scores; keeps reads in bounds
-            uint32_t val = bkey[tt] & ~31u;
-            const uint32_t oval = lane_xor32(val, hh);
-            const int ocw = (int)lane_xor32((uint32_t)cw, hh);
-            if (oval < val || (oval == val && ocw < cw)) {
-                val = oval;
-                cw = ocw;
-            }
-            if (hh == 0 && valid[tt]) {
-                if (GRP)
-                    symbols[srow[tt] * S + st] = (uint8_t)cw;
-                else
-                    sym_s[tok[tt] * S + st] = (uint8_t)cw;
-                if (ENC) sym_l[(tok[tt] - tb) * S + st] = (uint8_t)cw;
-            }
-            // next stage's bias: this stage's winning |u| grown by 2^-10
-            bz[tt] = bias_column(-__uint_as_float(val) * (1.0f + 0x1p-10f), hh);
-            // this lane's chunks of the chosen codeword
-            half8 cv[KS];
-            const uint8_t* crow = buf + (size_t)cw * C::ROW_P + hh * 16;
+            for (int tt = 0; tt < TT; ++tt) {
+                const int li = (int)(bkey[tt] & 31u);
+                int cw = (2 * bpair[tt] + (li >> 4)) * 32 + 8 * ((li & 15) >> 2) + 4 * hh + (li & 3);
+                cw = min(cw, K - 1);  // only reachable with all-NaN scores; keeps reads in bounds
+                uint32_t val = bkey[tt] & ~31u;
+                const uint32_t oval = lane_xor32(val, hh);
+                const int ocw = (int)lane_xor32((uint32_t)cw, hh);
+                if (oval < val || (oval == val && ocw < cw)) {
+                    val = oval;
+                    cw = ocw;
+                }
+                if (hh == 0 && valid[tt]) {
+                    if (GRP)
+                        symbols[srow[tt] * S + st] = (uint8_t)cw;
+                    else
+                        sym_s[tok[tt] * S + st] = (uint8_t)cw;
+                    if (ENC) sym_l[(tok[tt] - tb) * S + st] = (uint8_t)cw;
+                }
+                // next stage's bias: this stage's winning |u| grown by 2^-10
+                bz[tt] = bias_column(-__uint_as_float(val) * (1.0f + 0x1p-10f), hh);
+                // this lane's chunks of the chosen codeword
+                half8 cv[KS];
+                const uint8_t* crow = buf + (size_t)cw * C::ROW_P + hh * 16;
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) cv[ks] = *(const half8*)(crow + ks * 32);
-            const bool last = st + 1 == NS;
-            if (HILO && TWO && !last) {
-                // r = (hi + lo) - c for st >= 2, (x - c_0) - c_1 for st == 1; split again
+                for (int ks = 0; ks < KS; ++ks) cv[ks] = *(const half8*)(crow + ks * 32);
+                const bool last = st + 1 == NS;
+                if (HILO && TWO && !last) {
+                    // r = (hi + lo) - c for st >= 2, (x - c_0) - c_1 for st == 1; split again
 #pragma unroll
-                for (int ks = 0; ks < KS; ++ks) {
-                    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-                    const u32x4 a = __builtin_bit_cast(u32x4, bA[tt][ks]), b = __builtin_bit_cast(u32x4, bB[tt][ks]),
-                                c = __builtin_bit_cast(u32x4, cv[ks]);
-                    u32x4 na, nb;
+                    for (int ks = 0; ks < KS; ++ks) {
+                        typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+                        const u32x4 a = __builtin_bit_cast(u32x4, bA[tt][ks]), b = __builtin_bit_cast(u32x4, bB[tt][ks]),
+                                    c = __builtin_bit_cast(u32x4, cv[ks]);
+                        u32x4 na, nb;
 #pragma unroll
-                    for (int w = 0; w < 4; ++w) {
-                        uint32_t x, y;
-                        resplit2(a[w], b[w], c[w], x, y);
-                        na[w] = x;
-                        nb[w] = y;
+                        for (int w = 0; w < 4; ++w) {
+                            uint32_t x, y;
+                            resplit2(a[w], b[w], c[w], x, y);
+                            na[w] = x;
+                            nb[w] = y;
+                        }
+                        bA[tt][ks] = __builtin_bit_cast(half8, na);
+                        bB[tt][ks] = __builtin_bit_cast(half8, nb);
                     }
-                    bA[tt][ks] = __builtin_bit_cast(half8, na);
-                    bB[tt][ks] = __builtin_bit_cast(half8, nb);
+                }
+                if (last && residual && valid[tt]) {
+                    float* out = residual + (GRP ? srow[tt] : s * Ta + tok[tt]) * D + 8 * hh;
+#pragma unroll
+                    for (int ks = 0; ks < KS; ++ks) {
+                        floatx4 lo4, hi4;
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) {
+                            const float rv = (float)bA[tt][ks][e] + (TWO ? (float)bB[tt][ks][e] : 0.0f) -
+                                             (float)cv[ks][e];
+                            if (e < 4) lo4[e] = rv; else hi4[e - 4] = rv;
+                        }
+                        *(floatx4*)(out + 16 * ks) = lo4;
+                        *(floatx4*)(out + 16 * ks + 4) = hi4;
+                    }
+                }
+                if (!TWO && !last) {
+#pragma unroll
+                    for (int ks = 0; ks < KS; ++ks) bB[tt][ks] = -cv[ks];
                 }
             }
-            if (last && residual && valid[tt]) {
-                float* out = residual + (GRP ? srow[tt] : s * Ta + tok[tt]) * D + 8 * hh;
-#pragma unroll
-                for (int ks = 0; ks < KS; ++ks) {
-                    floatx4 lo4, hi4;
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        const float rv = (float)bA[tt][ks][e] + (TWO ? (float)bB[tt][ks][e] : 0.0f) -
-                                         (float)cv[ks][e];
-                        if (e < 4) lo4[e] = rv; else hi4[e - 4] = rv;
-                    }
-                    *(floatx4*)(out + 16 * ks) = lo4;
-                    *(floatx4*)(out + 16 * ks + 4) = hi4;
-                }
-            }
-            if (!TWO && !last) {
-#pragma unroll
-                for (int ks = 0; ks < KS; ++ks) bB[tt][ks] = -cv[ks];
-            }
-        }
         }   // wave_on
         if (st + 1 < NS && (NBUF == 1 || st >= 1 || st + 2 < NS)) {
             // Book pipeline: buffer `cur` is free once every wave is past here.
@@ -589,7 +589,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
             }
             __syncthreads();
         }
-        };
+    };
     stage(0, std::false_type{});
     for (int st = 1; st < NS; ++st) stage(st, std::true_type{});
     if (ENC) {
@@ -805,7 +805,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, kSmallBlocks) void rvq_small_kerne
 #pragma unroll
                 for (int ks = 0; ks < KS; ++ks) bB[0][ks] = -cv[ks];
             }
-                };
+        };
         stage(0, std::false_type{});
         if (NS > 1) stage(1, std::true_type{});
     };
