@@ -15,8 +15,10 @@
  *   - Device pointers are plain device addresses owned by the caller (for
  *     example PyTorch tensors); the library never allocates, frees or
  *     synchronises in these calls, and keeps no global mutable state, so
- *     calls are re-entrant.  `stream` is a hipStream_t (NULL = the null
- *     stream); all device work is enqueued on it asynchronously.
+ *     calls are re-entrant -- except fkv_kmeans_update_noalloc, whose device
+ *     scratch array is shared by every call on one device (see its comment).
+ *     `stream` is a hipStream_t (NULL = the null stream); all device work is
+ *     enqueued on it asynchronously.
  *   - Arguments are validated on the host before anything is enqueued.  An
  *     invalid call returns a negative fkv_status and has no side effect.
  *   - Data-dependent outcomes (a span failing its anchor check, an
