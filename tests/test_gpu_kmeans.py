@@ -32,6 +32,26 @@ def test_lloyd_iterations_match_oracle(fkv, orc, name):
             assert np.array_equal(host(bd).view(np.uint16), want.view(np.uint16)), (it, stage)
 
 
+@pytest.mark.parametrize("d,S,K", [(64, 8, 32), (128, 3, 256), (48, 6, 20)])
+def test_every_stage_matches_oracle(fkv, orc, d, S, K):
+    """One update of every stage of deep books: stages 0-4 run kernels with the stage fixed at compile
+    time, stages 5-7 the one that takes it at run time; each must match the oracle bit for bit."""
+    rng = np.random.default_rng(d + S + K)
+    ns, T, nb = 6, 120, 3
+    x = (rng.standard_normal((ns, T, d)) * 1.3).astype(np.float16)
+    books = (rng.standard_normal((nb, S, K, d)) * (0.6 ** np.arange(S))[None, :, None, None]).astype(np.float16)
+    sb = rng.integers(0, nb, ns).astype(np.int32)
+    xd, bd, sd = (torch.from_numpy(a).cuda() for a in (x, books, sb))
+    sym, _ = fkv.fkv_rvq_assign(xd, bd, sd, 2, T - 1)
+    symh = host(sym)
+    for stage in range(S):
+        before = host(bd).copy()
+        _, counts = fkv.fkv_kmeans_step(xd, bd, sd, 2, T - 1, sym, stage)
+        want, _, wc = orc.kmeans_update(x, before, sb, 2, T - 1, symh, stage)
+        assert np.array_equal(host(counts), wc), stage
+        assert np.array_equal(host(bd).view(np.uint16), want.view(np.uint16)), stage
+
+
 def test_skipped_tokens(fkv, orc):
     """Streams with an invalid book id and tokens whose symbols reach K contribute nothing."""
     rng = np.random.default_rng(4)
