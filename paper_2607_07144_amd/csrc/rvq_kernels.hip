@@ -357,10 +357,16 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
     float* __restrict__ residual, uint32_t* __restrict__ n_bad, int64_t T, int64_t t_begin,
     int64_t Ta, int S, int NS, int K, int Kp, int n_books, int64_t blocks_per_stream, int64_t tpb,
     double2* __restrict__ points, const double2* __restrict__ vtab, double cr, int cN, int cL, int64_t n_spans,
-    const int32_t* __restrict__ groups, int G, int64_t n_streams)
+    const int32_t* __restrict__ groups, int G, int64_t n_streams, int64_t ipb, int64_t n_items)
 {
     static_assert(!(GRP && ENC), "the grouped form has no fused encode");
     using C = Cfg<D>;
+    // PERS: a block takes ipb consecutive work items (token ranges, mostly of
+    // one stream) and loads the next item's token rows into registers during
+    // the current item's last stage, so a new item does not start by waiting
+    // on HBM.  Only the hi/lo per-stream instances hold the extra registers
+    // without spilling.
+    constexpr bool PERS = HILO && !ENC && !GRP;
     constexpr int KS = C::KS, TT = C::TT, TOK = C::TOK, NBUF = C::NBUF;
     extern __shared__ __align__(16) uint8_t lds[];
     // LDS: NBUF buffers of Kp rows (codeword + bias-step chunk) and a zero
@@ -371,258 +377,286 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, Cfg<D>::MIN_BLOCKS) void rvq_assig
     // work items, so the blocks of one stream share that XCD's L2 copy of its book.
     const uint32_t nblk = gridDim.x, q8 = nblk / 8, r8 = nblk % 8;
     const uint32_t xcd = blockIdx.x % 8, slot = blockIdx.x / 8;
-    const int64_t item = (int64_t)xcd * q8 + min(xcd, r8) + slot;
-    const int64_t s = item / blocks_per_stream;                // the stream (GRP: the group)
-    const int64_t Tv = GRP ? (int64_t)G * Ta : Ta;             // the item's tokens
-    const int64_t tb = (item - s * blocks_per_stream) * tpb;   // first token of the block
-    const int64_t te = min(Tv, tb + tpb);                      // one past its last
-
+    const int64_t bidx = (int64_t)xcd * q8 + min(xcd, r8) + slot;
+    const int64_t it0 = PERS ? bidx * ipb : bidx;
+    const int64_t it1 = PERS ? min(it0 + ipb, n_items) : it0 + 1;
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int col = lane & 31, hh = lane >> 5;
-    uint8_t* sym_s = symbols + s * Ta * S;
-    int b = GRP ? -1 : stream_book[s];
+    half8 bN[TT][KS];   // PERS: the next item's token rows
+    bool have_next = false;
+    for (int64_t item = it0; item < it1; ++item) {
+        const int64_t s = item / blocks_per_stream;                // the stream (GRP: the group)
+        const int64_t Tv = GRP ? (int64_t)G * Ta : Ta;             // the item's tokens
+        const int64_t tb = (item - s * blocks_per_stream) * tpb;   // first token of the block
+        const int64_t te = min(Tv, tb + tpb);                      // one past its last
 
-    // this lane's tokens (independent of the book id, so their loads overlap its)
-    int64_t tok[TT];
-    bool valid[TT];
-    int64_t srow[TT];               // GRP: the token's row in the [n_streams][Ta] outputs
-    half8 bA[TT][KS], bB[TT][KS];   // B operands of the current stage's passes
-    half8 bz[TT];                   // bias-step B operand
-#pragma unroll
-    for (int tt = 0; tt < TT; ++tt) {
-        tok[tt] = tb + (int64_t)(wave * TT + tt) * 32 + col;
-        valid[tt] = tok[tt] < te;
-        int64_t xr;
-        if constexpr (GRP) {
-            // member e's token t; a member id out of range rejects the group
-            // below, and meanwhile reads stream 0
-            const int64_t tv = valid[tt] ? tok[tt] : tb;
-            const int64_t e = tv / Ta, t = tv - e * Ta;
-            const int64_t m = groups[s * G + e];
-            const int64_t mm = (m >= 0 && m < n_streams) ? m : 0;
-            srow[tt] = mm * Ta + t;
-            xr = mm * T + t_begin + t;
-        } else {
-            srow[tt] = 0;
-            xr = s * T + t_begin + (valid[tt] ? tok[tt] : 0);
-        }
-        const _Float16* row = x + xr * D + 8 * hh;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            bA[tt][ks] = valid[tt] ? *(const half8*)(row + 16 * ks) : (half8)(_Float16)0;
-            bB[tt][ks] = (half8)(_Float16)0;
-        }
-    }
-    if constexpr (GRP) {
-        // the group's book: its first member's, which every member must share
-        const int32_t m0 = groups[s * G];
-        const int gb = (m0 >= 0 && m0 < n_streams) ? stream_book[m0] : -1;
-        int bad = gb < 0 || gb >= n_books;
-        if (tid < G) {
-            const int32_t m = groups[s * G + tid];
-            bad |= m < 0 || m >= n_streams || stream_book[m] != gb;
-        }
-        b = __syncthreads_or(bad) ? -1 : gb;
-    }
+        uint8_t* sym_s = symbols + s * Ta * S;
+        int b = GRP ? -1 : stream_book[s];
 
-    if (b < 0 || b >= n_books) {
-        if constexpr (GRP) {
-            // every in-range member's symbols (and residual) of the block's tokens
-            for (int64_t i = tb * S + tid; i < te * S; i += C::THREADS) {
-                const int64_t j = i / S, e = j / Ta, m = groups[s * G + e];
-                if (m >= 0 && m < n_streams) symbols[(m * Ta + (j - e * Ta)) * S + (i - j * S)] = 0xFF;
-            }
-            if (residual)
-                for (int64_t i = tb * D + tid; i < te * D; i += C::THREADS) {
-                    const int64_t j = i / D, e = j / Ta, m = groups[s * G + e];
-                    if (m >= 0 && m < n_streams) residual[(m * Ta + (j - e * Ta)) * D + (i - j * D)] = NAN;
-                }
-            if (tid == 0 && tb == 0 && n_bad) atomicAdd(n_bad, 1u);
-            return;
-        }
-        for (int64_t i = tb * S + tid; i < te * S; i += C::THREADS) sym_s[i] = 0xFF;
-        if (ENC)   // the block's spans encode 0xFF symbols: NaN points, as a separate encode gives
-            for (int64_t j = tb * S / cL + tid; j < (te * S + cL - 1) / cL; j += C::THREADS)
-                points[s * n_spans + j] = make_double2(NAN, NAN);
-        if (residual)
-            for (int64_t i = tb * D + tid; i < te * D; i += C::THREADS) residual[s * Ta * D + i] = NAN;
-        if (tid == 0 && tb == 0 && n_bad) atomicAdd(n_bad, 1u);
-        return;
-    }
-    const _Float16* bk = books + (int64_t)b * S * K * D;
-
-    // Fused span encode: the vertex table (NaN beyond the alphabet) and the
-    // block's symbols live after the book buffers.
-    double2* V_l = (double2*)(lds + NBUF * buf_bytes);
-    uint8_t* sym_l = (uint8_t*)(V_l + 256);
-    if (ENC && tid < 256) V_l[tid] = tid < cN ? vtab[tid] : make_double2(NAN, NAN);
-
-    // start the first books' copies; zero the buffers' end pads
-    book_to_lds_async<D>(bk, K, Kp, lds, wave, lane);
-    if (NBUF > 1 && NS > 1) book_to_lds_async<D>(bk + (size_t)K * D, K, Kp, lds + buf_bytes, wave, lane);
-    if (tid < NBUF) *(half8*)(lds + tid * buf_bytes + (size_t)Kp * C::ROW_P) = (half8)(_Float16)0;
-
-#pragma unroll
-    for (int tt = 0; tt < TT; ++tt) {
-        float n2 = 0.0f;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-#pragma unroll
-            for (int e = 0; e < 8; e += 2) {
-                const half2 h = {bA[tt][ks][e], bA[tt][ks][e + 1]};
-                n2 = __builtin_amdgcn_fdot2(h, h, n2, false);
-            }
-        }
-        n2 += __uint_as_float(lane_xor32(__float_as_uint(n2), hh));
-        bz[tt] = bias_column(0.5f * n2 * (1.0f + 0x1p-10f), hh);
-    }
-    const uint32_t fa = (uint32_t)(col * C::ROW_P + hh * 16);
-
-    wait_all_and_sync();
-    if (NBUF > 1 && NS > 1)
-        book_bias_rows<D, 2>(lds, lds + buf_bytes, Kp);
-    else
-        book_bias_rows<D, 1>(lds, lds, Kp);
-    __syncthreads();
-
-    const int nct = Kp / 32;  // even
-    // GRP: a wave without tokens (short items, such as one token per member)
-    // skips the scans and only takes part in the book pipeline
-    const bool wave_on = !GRP || __builtin_amdgcn_readfirstlane((int)(tb + (int64_t)wave * TT * 32 < te));
-    // One stage: TWO (stages 1..) scans with two passes per tile.  Stage 0 is
-    // issued on its own, ahead of the loop over the later stages: with one
-    // loop body holding both scan forms the register allocator kept both
-    // forms' values live across the loop and spilled (d = 128, three stages:
-    // 256 VGPRs and 32 bytes of scratch per lane, against 188 and none).
-    auto stage = [&](const int st, auto two_c) {
-        constexpr bool TWO = decltype(two_c)::value;
-        const int cur = NBUF > 1 ? (st & 1) : 0;
-        const uint8_t* buf = lds + cur * buf_bytes;
-        uint32_t bkey[TT];
-        int bpair[TT];
+        // this lane's tokens (independent of the book id, so their loads overlap its)
+        int64_t tok[TT];
+        bool valid[TT];
+        int64_t srow[TT];               // GRP: the token's row in the [n_streams][Ta] outputs
+        half8 bA[TT][KS], bB[TT][KS];   // B operands of the current stage's passes
+        half8 bz[TT];                   // bias-step B operand
+        const bool prefetched = PERS && have_next;
+        have_next = false;
 #pragma unroll
         for (int tt = 0; tt < TT; ++tt) {
-            bkey[tt] = 0xFFFFFFFFu;
-            bpair[tt] = 0;
+            tok[tt] = tb + (int64_t)(wave * TT + tt) * 32 + col;
+            valid[tt] = tok[tt] < te;
+            int64_t xr;
+            if constexpr (GRP) {
+                // member e's token t; a member id out of range rejects the group
+                // below, and meanwhile reads stream 0
+                const int64_t tv = valid[tt] ? tok[tt] : tb;
+                const int64_t e = tv / Ta, t = tv - e * Ta;
+                const int64_t m = groups[s * G + e];
+                const int64_t mm = (m >= 0 && m < n_streams) ? m : 0;
+                srow[tt] = mm * Ta + t;
+                xr = mm * T + t_begin + t;
+            } else {
+                srow[tt] = 0;
+                xr = s * T + t_begin + (valid[tt] ? tok[tt] : 0);
+            }
+            const _Float16* row = x + xr * D + 8 * hh;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                if (prefetched)
+                    bA[tt][ks] = bN[tt][ks];
+                else
+                    bA[tt][ks] = valid[tt] ? *(const half8*)(row + 16 * ks) : (half8)(_Float16)0;
+                bB[tt][ks] = (half8)(_Float16)0;
+            }
         }
-        if (wave_on) {
-            stage_scan<D, TT, TWO>(buf, fa, nct, bz, bA, bB, bkey, bpair);
+        if constexpr (GRP) {
+            // the group's book: its first member's, which every member must share
+            const int32_t m0 = groups[s * G];
+            const int gb = (m0 >= 0 && m0 < n_streams) ? stream_book[m0] : -1;
+            int bad = gb < 0 || gb >= n_books;
+            if (tid < G) {
+                const int32_t m = groups[s * G + tid];
+                bad |= m < 0 || m >= n_streams || stream_book[m] != gb;
+            }
+            b = __syncthreads_or(bad) ? -1 : gb;
+        }
+
+        if (b < 0 || b >= n_books) {
+            if constexpr (GRP) {
+                // every in-range member's symbols (and residual) of the block's tokens
+                for (int64_t i = tb * S + tid; i < te * S; i += C::THREADS) {
+                    const int64_t j = i / S, e = j / Ta, m = groups[s * G + e];
+                    if (m >= 0 && m < n_streams) symbols[(m * Ta + (j - e * Ta)) * S + (i - j * S)] = 0xFF;
+                }
+                if (residual)
+                    for (int64_t i = tb * D + tid; i < te * D; i += C::THREADS) {
+                        const int64_t j = i / D, e = j / Ta, m = groups[s * G + e];
+                        if (m >= 0 && m < n_streams) residual[(m * Ta + (j - e * Ta)) * D + (i - j * D)] = NAN;
+                    }
+                if (tid == 0 && tb == 0 && n_bad) atomicAdd(n_bad, 1u);
+                return;
+            }
+            for (int64_t i = tb * S + tid; i < te * S; i += C::THREADS) sym_s[i] = 0xFF;
+            if (ENC)   // the block's spans encode 0xFF symbols: NaN points, as a separate encode gives
+                for (int64_t j = tb * S / cL + tid; j < (te * S + cL - 1) / cL; j += C::THREADS)
+                    points[s * n_spans + j] = make_double2(NAN, NAN);
+            if (residual)
+                for (int64_t i = tb * D + tid; i < te * D; i += C::THREADS) residual[s * Ta * D + i] = NAN;
+            if (tid == 0 && tb == 0 && n_bad) atomicAdd(n_bad, 1u);
+            continue;
+        }
+        const _Float16* bk = books + (int64_t)b * S * K * D;
+
+        // Fused span encode: the vertex table (NaN beyond the alphabet) and the
+        // block's symbols live after the book buffers.
+        double2* V_l = (double2*)(lds + NBUF * buf_bytes);
+        uint8_t* sym_l = (uint8_t*)(V_l + 256);
+        if (ENC && tid < 256) V_l[tid] = tid < cN ? vtab[tid] : make_double2(NAN, NAN);
+
+        // start the first books' copies; zero the buffers' end pads
+        book_to_lds_async<D>(bk, K, Kp, lds, wave, lane);
+        if (NBUF > 1 && NS > 1) book_to_lds_async<D>(bk + (size_t)K * D, K, Kp, lds + buf_bytes, wave, lane);
+        if (tid < NBUF) *(half8*)(lds + tid * buf_bytes + (size_t)Kp * C::ROW_P) = (half8)(_Float16)0;
+
+#pragma unroll
+        for (int tt = 0; tt < TT; ++tt) {
+            float n2 = 0.0f;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+#pragma unroll
+                for (int e = 0; e < 8; e += 2) {
+                    const half2 h = {bA[tt][ks][e], bA[tt][ks][e + 1]};
+                    n2 = __builtin_amdgcn_fdot2(h, h, n2, false);
+                }
+            }
+            n2 += __uint_as_float(lane_xor32(__float_as_uint(n2), hh));
+            bz[tt] = bias_column(0.5f * n2 * (1.0f + 0x1p-10f), hh);
+        }
+        const uint32_t fa = (uint32_t)(col * C::ROW_P + hh * 16);
+
+        wait_all_and_sync();
+        if (NBUF > 1 && NS > 1)
+            book_bias_rows<D, 2>(lds, lds + buf_bytes, Kp);
+        else
+            book_bias_rows<D, 1>(lds, lds, Kp);
+        __syncthreads();
+
+        const int nct = Kp / 32;  // even
+        // GRP: a wave without tokens (short items, such as one token per member)
+        // skips the scans and only takes part in the book pipeline
+        const bool wave_on = !GRP || __builtin_amdgcn_readfirstlane((int)(tb + (int64_t)wave * TT * 32 < te));
+        // One stage: TWO (stages 1..) scans with two passes per tile.  Stage 0 is
+        // issued on its own, ahead of the loop over the later stages: with one
+        // loop body holding both scan forms the register allocator kept both
+        // forms' values live across the loop and spilled (d = 128, three stages:
+        // 256 VGPRs and 32 bytes of scratch per lane, against 188 and none).
+        auto stage = [&](const int st, auto two_c) {
+            constexpr bool TWO = decltype(two_c)::value;
+            if (PERS && st + 1 == NS && item + 1 < it1) {
+                // the next item's token rows, in flight during this stage
+                const int64_t sn = (item + 1) / blocks_per_stream;
+                const int64_t tbn = (item + 1 - sn * blocks_per_stream) * tpb;
+                const int64_t ten = min(Ta, tbn + tpb);
+#pragma unroll
+                for (int tt = 0; tt < TT; ++tt) {
+                    const int64_t tk = tbn + (int64_t)(wave * TT + tt) * 32 + col;
+                    const bool v = tk < ten;
+                    const _Float16* row = x + (sn * T + t_begin + (v ? tk : 0)) * D + 8 * hh;
+#pragma unroll
+                    for (int ks = 0; ks < KS; ++ks)
+                        bN[tt][ks] = v ? *(const half8*)(row + 16 * ks) : (half8)(_Float16)0;
+                }
+                have_next = true;
+            }
+            const int cur = NBUF > 1 ? (st & 1) : 0;
+            const uint8_t* buf = lds + cur * buf_bytes;
+            uint32_t bkey[TT];
+            int bpair[TT];
 #pragma unroll
             for (int tt = 0; tt < TT; ++tt) {
-                const int li = (int)(bkey[tt] & 31u);
-                int cw = (2 * bpair[tt] + (li >> 4)) * 32 + 8 * ((li & 15) >> 2) + 4 * hh + (li & 3);
-                cw = min(cw, K - 1);  // only reachable with all-NaN scores; keeps reads in bounds
-                uint32_t val = bkey[tt] & ~31u;
-                const uint32_t oval = lane_xor32(val, hh);
-                const int ocw = (int)lane_xor32((uint32_t)cw, hh);
-                if (oval < val || (oval == val && ocw < cw)) {
-                    val = oval;
-                    cw = ocw;
-                }
-                if (hh == 0 && valid[tt]) {
-                    if (GRP)
-                        symbols[srow[tt] * S + st] = (uint8_t)cw;
-                    else
-                        sym_s[tok[tt] * S + st] = (uint8_t)cw;
-                    if (ENC) sym_l[(tok[tt] - tb) * S + st] = (uint8_t)cw;
-                }
-                // next stage's bias: this stage's winning |u| grown by 2^-10
-                bz[tt] = bias_column(-__uint_as_float(val) * (1.0f + 0x1p-10f), hh);
-                // this lane's chunks of the chosen codeword
-                half8 cv[KS];
-                const uint8_t* crow = buf + (size_t)cw * C::ROW_P + hh * 16;
-#pragma unroll
-                for (int ks = 0; ks < KS; ++ks) cv[ks] = *(const half8*)(crow + ks * 32);
-                const bool last = st + 1 == NS;
-                if (HILO && TWO && !last) {
-                    // r = (hi + lo) - c for st >= 2, (x - c_0) - c_1 for st == 1; split again
-#pragma unroll
-                    for (int ks = 0; ks < KS; ++ks) {
-                        typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-                        const u32x4 a = __builtin_bit_cast(u32x4, bA[tt][ks]), b = __builtin_bit_cast(u32x4, bB[tt][ks]),
-                                    c = __builtin_bit_cast(u32x4, cv[ks]);
-                        u32x4 na, nb;
-#pragma unroll
-                        for (int w = 0; w < 4; ++w) {
-                            uint32_t x, y;
-                            resplit2(a[w], b[w], c[w], x, y);
-                            na[w] = x;
-                            nb[w] = y;
-                        }
-                        bA[tt][ks] = __builtin_bit_cast(half8, na);
-                        bB[tt][ks] = __builtin_bit_cast(half8, nb);
-                    }
-                }
-                if (last && residual && valid[tt]) {
-                    float* out = residual + (GRP ? srow[tt] : s * Ta + tok[tt]) * D + 8 * hh;
-#pragma unroll
-                    for (int ks = 0; ks < KS; ++ks) {
-                        floatx4 lo4, hi4;
-#pragma unroll
-                        for (int e = 0; e < 8; ++e) {
-                            const float rv = (float)bA[tt][ks][e] + (TWO ? (float)bB[tt][ks][e] : 0.0f) -
-                                             (float)cv[ks][e];
-                            if (e < 4) lo4[e] = rv; else hi4[e - 4] = rv;
-                        }
-                        *(floatx4*)(out + 16 * ks) = lo4;
-                        *(floatx4*)(out + 16 * ks + 4) = hi4;
-                    }
-                }
-                if (!TWO && !last) {
-#pragma unroll
-                    for (int ks = 0; ks < KS; ++ks) bB[tt][ks] = -cv[ks];
-                }
+                bkey[tt] = 0xFFFFFFFFu;
+                bpair[tt] = 0;
             }
-        }   // wave_on
-        if (st + 1 < NS && (NBUF == 1 || st >= 1 || st + 2 < NS)) {
-            // Book pipeline: buffer `cur` is free once every wave is past here.
-            wait_all_and_sync();
-            if (NBUF == 1) {
-                book_to_lds_async<D>(bk + (size_t)(st + 1) * K * D, K, Kp, lds, wave, lane);
+            if (wave_on) {
+                stage_scan<D, TT, TWO>(buf, fa, nct, bz, bA, bB, bkey, bpair);
+#pragma unroll
+                for (int tt = 0; tt < TT; ++tt) {
+                    const int li = (int)(bkey[tt] & 31u);
+                    int cw = (2 * bpair[tt] + (li >> 4)) * 32 + 8 * ((li & 15) >> 2) + 4 * hh + (li & 3);
+                    cw = min(cw, K - 1);  // only reachable with all-NaN scores; keeps reads in bounds
+                    uint32_t val = bkey[tt] & ~31u;
+                    const uint32_t oval = lane_xor32(val, hh);
+                    const int ocw = (int)lane_xor32((uint32_t)cw, hh);
+                    if (oval < val || (oval == val && ocw < cw)) {
+                        val = oval;
+                        cw = ocw;
+                    }
+                    if (hh == 0 && valid[tt]) {
+                        if (GRP)
+                            symbols[srow[tt] * S + st] = (uint8_t)cw;
+                        else
+                            sym_s[tok[tt] * S + st] = (uint8_t)cw;
+                        if (ENC) sym_l[(tok[tt] - tb) * S + st] = (uint8_t)cw;
+                    }
+                    // next stage's bias: this stage's winning |u| grown by 2^-10
+                    bz[tt] = bias_column(-__uint_as_float(val) * (1.0f + 0x1p-10f), hh);
+                    // this lane's chunks of the chosen codeword
+                    half8 cv[KS];
+                    const uint8_t* crow = buf + (size_t)cw * C::ROW_P + hh * 16;
+#pragma unroll
+                    for (int ks = 0; ks < KS; ++ks) cv[ks] = *(const half8*)(crow + ks * 32);
+                    const bool last = st + 1 == NS;
+                    if (HILO && TWO && !last) {
+                        // r = (hi + lo) - c for st >= 2, (x - c_0) - c_1 for st == 1; split again
+#pragma unroll
+                        for (int ks = 0; ks < KS; ++ks) {
+                            typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+                            const u32x4 a = __builtin_bit_cast(u32x4, bA[tt][ks]), b = __builtin_bit_cast(u32x4, bB[tt][ks]),
+                                        c = __builtin_bit_cast(u32x4, cv[ks]);
+                            u32x4 na, nb;
+#pragma unroll
+                            for (int w = 0; w < 4; ++w) {
+                                uint32_t x, y;
+                                resplit2(a[w], b[w], c[w], x, y);
+                                na[w] = x;
+                                nb[w] = y;
+                            }
+                            bA[tt][ks] = __builtin_bit_cast(half8, na);
+                            bB[tt][ks] = __builtin_bit_cast(half8, nb);
+                        }
+                    }
+                    if (last && residual && valid[tt]) {
+                        float* out = residual + (GRP ? srow[tt] : s * Ta + tok[tt]) * D + 8 * hh;
+#pragma unroll
+                        for (int ks = 0; ks < KS; ++ks) {
+                            floatx4 lo4, hi4;
+#pragma unroll
+                            for (int e = 0; e < 8; ++e) {
+                                const float rv = (float)bA[tt][ks][e] + (TWO ? (float)bB[tt][ks][e] : 0.0f) -
+                                                 (float)cv[ks][e];
+                                if (e < 4) lo4[e] = rv; else hi4[e - 4] = rv;
+                            }
+                            *(floatx4*)(out + 16 * ks) = lo4;
+                            *(floatx4*)(out + 16 * ks + 4) = hi4;
+                        }
+                    }
+                    if (!TWO && !last) {
+#pragma unroll
+                        for (int ks = 0; ks < KS; ++ks) bB[tt][ks] = -cv[ks];
+                    }
+                }
+            }   // wave_on
+            if (st + 1 < NS && (NBUF == 1 || st >= 1 || st + 2 < NS)) {
+                // Book pipeline: buffer `cur` is free once every wave is past here.
                 wait_all_and_sync();
-            } else if (st + 2 < NS) {
-                book_to_lds_async<D>(bk + (size_t)(st + 2) * K * D, K, Kp, lds + cur * buf_bytes, wave, lane);
+                if (NBUF == 1) {
+                    book_to_lds_async<D>(bk + (size_t)(st + 1) * K * D, K, Kp, lds, wave, lane);
+                    wait_all_and_sync();
+                } else if (st + 2 < NS) {
+                    book_to_lds_async<D>(bk + (size_t)(st + 2) * K * D, K, Kp, lds + cur * buf_bytes, wave, lane);
+                }
+                if (NBUF == 1 || st >= 1) {
+                    uint8_t* nb = lds + (NBUF > 1 ? ((st + 1) & 1) : 0) * buf_bytes;
+                    book_bias_rows<D, 1>(nb, nb, Kp);
+                }
+                __syncthreads();
             }
-            if (NBUF == 1 || st >= 1) {
-                uint8_t* nb = lds + (NBUF > 1 ? ((st + 1) & 1) : 0) * buf_bytes;
-                book_bias_rows<D, 1>(nb, nb, Kp);
-            }
+        };
+        stage(0, std::false_type{});
+        for (int st = 1; st < NS; ++st) stage(st, std::true_type{});
+        if (ENC) {
+            // Span encode of the block's symbols (Sec. 1 "The code"): the block's
+            // token range holds whole spans, each walked from the anchor (0,0) with
+            // p <- V + r (p - V), operation for operation as the encode kernel, and
+            // stored with a streaming store (measured: faster on the four-stage
+            // d = 64 shape, neutral elsewhere; slower in the small-book kernel).
             __syncthreads();
-        }
-    };
-    stage(0, std::false_type{});
-    for (int st = 1; st < NS; ++st) stage(st, std::true_type{});
-    if (ENC) {
-        // Span encode of the block's symbols (Sec. 1 "The code"): the block's
-        // token range holds whole spans, each walked from the anchor (0,0) with
-        // p <- V + r (p - V), operation for operation as the encode kernel, and
-        // stored with a streaming store (measured: faster on the four-stage
-        // d = 64 shape, neutral elsewhere; slower in the small-book kernel).
-        __syncthreads();
-        const int64_t n_sym = Ta * S;
-        for (int64_t j = tb * S / cL + tid; j < (te * S + cL - 1) / cL; j += C::THREADS) {
-            const int64_t a = j * cL;
-            const int len = (int)min((int64_t)cL, n_sym - a);
-            const uint8_t* my = sym_l + (a - tb * S);
-            double px = 0.0, py = 0.0;
-            for (int k0 = 0; k0 < len; k0 += 8) {
-                // the vertices of up to 8 symbols first (they do not depend on p),
-                // then the dependent steps
-                double2 v[8];
+            const int64_t n_sym = Ta * S;
+            for (int64_t j = tb * S / cL + tid; j < (te * S + cL - 1) / cL; j += C::THREADS) {
+                const int64_t a = j * cL;
+                const int len = (int)min((int64_t)cL, n_sym - a);
+                const uint8_t* my = sym_l + (a - tb * S);
+                double px = 0.0, py = 0.0;
+                for (int k0 = 0; k0 < len; k0 += 8) {
+                    // the vertices of up to 8 symbols first (they do not depend on p),
+                    // then the dependent steps
+                    double2 v[8];
 #pragma unroll
-                for (int u = 0; u < 8; ++u) v[u] = k0 + u < len ? V_l[my[k0 + u]] : make_double2(0.0, 0.0);
+                    for (int u = 0; u < 8; ++u) v[u] = k0 + u < len ? V_l[my[k0 + u]] : make_double2(0.0, 0.0);
 #pragma unroll
-                for (int u = 0; u < 8; ++u) {
-                    if (k0 + u < len) {
-                        const double tx = px - v[u].x, ty = py - v[u].y;
-                        const double ux = cr * tx, uy = cr * ty;
-                        px = v[u].x + ux;
-                        py = v[u].y + uy;
+                    for (int u = 0; u < 8; ++u) {
+                        if (k0 + u < len) {
+                            const double tx = px - v[u].x, ty = py - v[u].y;
+                            const double ux = cr * tx, uy = cr * ty;
+                            px = v[u].x + ux;
+                            py = v[u].y + uy;
+                        }
                     }
                 }
+                store_point_stream(points + s * n_spans + j, px, py);
             }
-            store_point_stream(points + s * n_spans + j, px, py);
         }
+        if (item + 1 < it1) __syncthreads();   // the next item's book copies overwrite the buffers
     }
 }
 
@@ -889,14 +923,18 @@ int launch_rvq_t(const fkv_rvq_desc* dsc, int ns, const uint16_t* x, const uint1
     }
     const int64_t items = GRP ? grp.n_groups : dsc->n_streams;
     const int64_t bps = ((GRP ? grp.G * Ta : Ta) + tpb - 1) / tpb;
-    const int64_t nblk = bps * items;
+    const int64_t n_items = bps * items;
+    // 16 items per block once there are at least 64 blocks' worth per compute
+    // unit (2-3.5% faster at the long-context shape than one item per block)
+    const int64_t ipb = (HILO && !ENC && !GRP && n_items >= 256 * 64) ? 16 : 1;
+    const int64_t nblk = (n_items + ipb - 1) / ipb;
     if (nblk > 0x7fffffff) return FKV_ERR_UNSUPPORTED;
     const int64_t n_spans = ENC ? (Ta * dsc->S + enc.L - 1) / enc.L : 0;
     const size_t shm = lds_bytes<D>(Kp) + (ENC ? enc_lds_bytes<D>() : 0);
     hipLaunchKernelGGL((rvq_assign_kernel<D, HILO, ENC, GRP>), dim3((unsigned)nblk), dim3(Cfg<D>::THREADS), shm,
                        stream, (const _Float16*)x, (const _Float16*)books, stream_book, symbols, residual, n_bad,
                        dsc->T, dsc->t_begin, Ta, dsc->S, ns, dsc->K, Kp, dsc->n_books, bps, tpb, enc.points, enc.vtab,
-                       enc.r, enc.N, enc.L, n_spans, grp.groups, grp.G, dsc->n_streams);
+                       enc.r, enc.N, enc.L, n_spans, grp.groups, grp.G, dsc->n_streams, ipb, n_items);
     return launch_status();
 }
 
