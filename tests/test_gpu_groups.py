@@ -115,3 +115,31 @@ def test_eviction_step_matches_oracle(fkv, orc):
     assert np.abs(o["residual"] - res.astype(np.float64)).max() <= 1e-3
     print("eviction step: %d streams, %d groups of %d, near-ties accepted %d"
           % (x.shape[0], groups.shape[0], groups.shape[1], o["n_forced"]))
+
+
+def test_multi_item_blocks_match_single_item_blocks(fkv):
+    """At 2^14 and more work items the hi/lo per-stream form gives each block 16 consecutive items and
+    loads the next item's rows during the current item's last stage; the grouped form (one stream per
+    group) keeps one item per block with the same arithmetic.  Symbols, residuals and the invalid-stream
+    count must agree, with invalid streams between valid ones (an item that ends a block's run early)."""
+    rng = np.random.default_rng(11)
+    ns, T, d, S, K, nb = 128, 32800, 128, 3, 64, 4
+    t0, t1 = 4, 32772                                   # 32,768 tokens: 128 items of 256 per stream
+    x = torch.from_numpy((rng.standard_normal((ns, T, d)) * 1.2).astype(np.float16)).cuda()
+    books = torch.from_numpy((rng.standard_normal((nb, S, K, d)) *
+                              (0.5 ** np.arange(S))[None, :, None, None]).astype(np.float16)).cuda()
+    sbh = rng.integers(0, nb, ns).astype(np.int32)
+    sbh[[3, 40, 41, 127]] = 77                          # no valid book
+    sb = torch.from_numpy(sbh).cuda()
+    n1 = torch.zeros(1, dtype=torch.int32, device="cuda")
+    n2 = torch.zeros(1, dtype=torch.int32, device="cuda")
+    s1, r1 = fkv.fkv_rvq_assign(x, books, sb, t0, t1, want_residual=True, n_bad=n1)
+    groups = torch.arange(ns, dtype=torch.int32, device="cuda").view(ns, 1)
+    s2, r2 = fkv.fkv_rvq_assign_groups(x, books, sb, groups, t0, t1, want_residual=True, n_bad=n2)
+    assert int(n1.item()) == int(n2.item()) == 4
+    assert torch.equal(s1, s2)
+    a, b = host(r1), host(r2)
+    assert np.array_equal(np.isnan(a), np.isnan(b))
+    assert np.array_equal(np.nan_to_num(a).view(np.uint32), np.nan_to_num(b).view(np.uint32))
+    del x, s1, s2, r1, r2
+    torch.cuda.empty_cache()
