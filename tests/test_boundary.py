@@ -370,3 +370,19 @@ def test_noalloc_kmeans_rejects_inputs_beyond_its_scratch(F):
     assert lib.fkv_kmeans_update_noalloc(ctypes.byref(ok), None, p, p, p, 0, None, None) == F.FKV_ERR_INVALID_ARG
     bad = F.fkv_rvq_desc(288, 1024, 4, 992, 60, 2, 256, 288)
     assert lib.fkv_kmeans_update_noalloc(ctypes.byref(bad), p, p, p, p, 0, None, None) == F.FKV_ERR_INVALID_ARG
+
+
+def test_book_groups_host_helper(F):
+    """The host-side grouping the grouped assignment takes: each used book's streams in stream order."""
+    sb = np.array([2, 0, 2, 0, 1, 1], np.int32)
+    g = F.book_groups(sb)
+    assert g.dtype == np.int32 and g.tolist() == [[1, 3], [4, 5], [0, 2]]
+    from paper_2607_07144_amd import workloads as w
+    cfg = w.CONFIGS["long_gqa"]
+    sbl = w._stream_book(cfg, cfg.groups[0])
+    gl = F.book_groups(sbl)
+    assert gl.shape == (512, 4) and (sbl[gl] == sbl[gl[:, :1]]).all()
+    assert sorted(gl.ravel().tolist()) == list(range(2048))
+    with pytest.raises(ValueError):
+        F.book_groups(np.array([0, 0, 1], np.int32))
+    assert F.book_groups(np.zeros(0, np.int32)).shape[0] == 0
